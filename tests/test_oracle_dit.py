@@ -1,0 +1,317 @@
+"""Pins for the oracle denoiser (oracle/dit.py), CPU only.
+
+Each check is tied to something outside the oracle's own code: brute force
+loops, closed forms, invariants, or an independent formulation built from
+library routines (torch CPU functional ops in float64).
+"""
+import math
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as tF
+
+import synth
+from oracle import dit
+
+RNG = np.random.default_rng(1234)
+
+
+def small_cfg(**kw):
+    base = dict(name="unit", dtype="f32", hidden=64, heads=2, head_dim=32, n_seq=1, n_dual=1, n_single=1,
+                cond_dim=8, cam_dim=6, text_tokens=3, text_dim=10, latent=(16, 2, 4, 6),
+                patch=(1, 2, 2), rope=(8, 12, 12), steps=4, seed=7)
+    base.update(kw)
+    return synth.ModelConfig(**base)
+
+
+# --------------------------------------------------------------------------- elementary ops
+
+def test_layer_norm_matches_library_and_moments():
+    x = RNG.standard_normal((5, 48)) * 3 + 1
+    y = dit.layer_norm(x)
+    ref = tF.layer_norm(torch.tensor(x), (48,), eps=1e-6).numpy()
+    np.testing.assert_allclose(y, ref, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(y.mean(-1), 0, atol=1e-12)
+    np.testing.assert_allclose(y.var(-1), 1, atol=1e-5)
+
+
+def test_rms_norm_unit_rms_and_library():
+    x = RNG.standard_normal((4, 32)) * 5
+    y = dit.rms_norm(x)
+    np.testing.assert_allclose(np.sqrt((y * y).mean(-1)), 1, atol=1e-6)
+    ref = tF.rms_norm(torch.tensor(x), (32,), eps=1e-6).numpy()
+    np.testing.assert_allclose(y, ref, atol=1e-12)
+
+
+def test_gelu_tanh_matches_library():
+    x = np.linspace(-8, 8, 1001)
+    ref = tF.gelu(torch.tensor(x), approximate="tanh").numpy()
+    np.testing.assert_allclose(dit.gelu_tanh(x), ref, atol=1e-14)
+    assert dit.gelu_tanh(np.array([0.0]))[0] == 0.0
+
+
+def test_silu_closed_form():
+    x = np.linspace(-10, 10, 101)
+    np.testing.assert_allclose(dit.silu(x), tF.silu(torch.tensor(x)).numpy(), atol=1e-14)
+
+
+def test_timestep_features_closed_form():
+    f0 = dit.timestep_features(0.0)
+    np.testing.assert_array_equal(f0[:128], 1.0)
+    np.testing.assert_array_equal(f0[128:], 0.0)
+    t = 0.37
+    f = dit.timestep_features(t)
+    # j = 0 has frequency 1; j = 64 has frequency 1e4^(-1/2) = 0.01
+    assert f[0] == pytest.approx(math.cos(370.0), abs=1e-12)
+    assert f[128] == pytest.approx(math.sin(370.0), abs=1e-12)
+    assert f[64] == pytest.approx(math.cos(3.7), abs=1e-12)
+    assert f[192] == pytest.approx(math.sin(3.7), abs=1e-12)
+
+
+def test_linear_matches_library():
+    W = {"l.w": RNG.standard_normal((7, 5)), "l.b": RNG.standard_normal(7)}
+    x = RNG.standard_normal((3, 5))
+    ref = tF.linear(torch.tensor(x), torch.tensor(W["l.w"]), torch.tensor(W["l.b"])).numpy()
+    np.testing.assert_allclose(dit.linear(W, "l", x), ref, atol=1e-13)
+    np.testing.assert_allclose(dit.linear_rows(W, "l", x, 2, 5), ref[:, 2:5], atol=1e-13)
+
+
+# --------------------------------------------------------------------------- attention
+
+def brute_attention(q, k, v):
+    hh, nq, hd = q.shape
+    nk = k.shape[1]
+    out = np.zeros((hh, nq, v.shape[2]))
+    for h in range(hh):
+        for i in range(nq):
+            s = [sum(q[h, i, d] * k[h, j, d] for d in range(hd)) / math.sqrt(hd) for j in range(nk)]
+            m = max(s)
+            e = [math.exp(x - m) for x in s]
+            z = sum(e)
+            for j in range(nk):
+                for d in range(v.shape[2]):
+                    out[h, i, d] += e[j] / z * v[h, j, d]
+    return out
+
+
+def test_attention_brute_force():
+    q, k, v = (RNG.standard_normal((2, n, 8)) for n in (5, 7, 7))
+    np.testing.assert_allclose(dit.attention(q, k, v), brute_attention(q, k, v), atol=1e-12)
+
+
+def test_attention_chunking_does_not_change_result():
+    q, k, v = (RNG.standard_normal((3, 37, 16)) for _ in range(3))
+    np.testing.assert_allclose(dit.attention(q, k, v, chunk=5), dit.attention(q, k, v, chunk=1024), atol=1e-13)
+
+
+def test_attention_library_sdpa():
+    q, k, v = (RNG.standard_normal((4, 33, 64)) for _ in range(3))
+    ref = tF.scaled_dot_product_attention(torch.tensor(q), torch.tensor(k), torch.tensor(v)).numpy()
+    np.testing.assert_allclose(dit.attention(q, k, v), ref, atol=1e-12)
+
+
+def test_attention_special_cases():
+    # identical keys: every weight is 1/N, output = mean of V
+    q = RNG.standard_normal((1, 4, 8))
+    k = np.repeat(RNG.standard_normal((1, 1, 8)), 9, axis=1)
+    v = RNG.standard_normal((1, 9, 8))
+    np.testing.assert_allclose(dit.attention(q, k, v), np.broadcast_to(v.mean(1, keepdims=True), (1, 4, 8)), atol=1e-13)
+    # one dominant score selects that row of V
+    k2 = np.zeros((1, 6, 8)); k2[0, 3, 0] = 1e3
+    q2 = np.zeros((1, 1, 8)); q2[0, 0, 0] = 1.0
+    v2 = RNG.standard_normal((1, 6, 8))
+    np.testing.assert_allclose(dit.attention(q2, k2, v2)[0, 0], v2[0, 3], atol=1e-12)
+    # one vector added to every key adds q.c to a whole row of scores: no change (softmax shift)
+    q3, k3, v3 = (RNG.standard_normal((1, 5, 8)) for _ in range(3))
+    k3b = k3 + RNG.standard_normal((1, 1, 8))
+    np.testing.assert_allclose(dit.attention(q3, k3b, v3), dit.attention(q3, k3, v3), atol=1e-13)
+
+
+# --------------------------------------------------------------------------- RoPE
+
+def test_rope_matches_complex_rotation():
+    grid, dims = (2, 3, 4), (4, 6, 6)
+    ang = dit.rope_angles(grid, dims)
+    x = RNG.standard_normal((2, 24, 16))
+    y = dit.apply_rope(x, ang)
+    # independent formulation: pairs as complex numbers times e^{i*angle}
+    pos = [(f, h, w) for f in range(2) for h in range(3) for w in range(4)]
+    for n, (f, h, w) in enumerate(pos):
+        th = []
+        for p_, d in zip((f, h, w), dims):
+            th += [p_ * 10000.0 ** (-2.0 * j / d) for j in range(d // 2)]
+        zc = (x[:, n, 0::2] + 1j * x[:, n, 1::2]) * np.exp(1j * np.array(th))
+        np.testing.assert_allclose(y[:, n, 0::2], zc.real, atol=1e-12)
+        np.testing.assert_allclose(y[:, n, 1::2], zc.imag, atol=1e-12)
+
+
+def test_rope_invariants():
+    grid, dims = (3, 4, 5), (4, 6, 6)
+    ang = dit.rope_angles(grid, dims)
+    x = RNG.standard_normal((1, 60, 16))
+    y = dit.apply_rope(x, ang)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-12)
+    np.testing.assert_array_equal(y[:, 0], x[:, 0])          # position (0,0,0) is the identity
+    # <R_m q, R_n k> depends only on m - n (per axis): shift both tokens by one frame
+    q, k = RNG.standard_normal(16), RNG.standard_normal(16)
+    pos = dit.token_positions(grid)
+    idx = {tuple(p): i for i, p in enumerate(pos)}
+    def dot(a, b):
+        ra = dit.apply_rope(q[None], ang[[idx[a]]])[0]
+        rb = dit.apply_rope(k[None], ang[[idx[b]]])[0]
+        return ra @ rb
+    assert dot((0, 1, 2), (1, 3, 0)) == pytest.approx(dot((1, 1, 2), (2, 3, 0)), abs=1e-12)
+    assert dot((0, 0, 1), (0, 2, 4)) == pytest.approx(dot((0, 1, 0), (0, 3, 3)), abs=1e-12)
+
+
+# --------------------------------------------------------------------------- patches
+
+def test_patchify_layout_and_roundtrip():
+    z = RNG.standard_normal((16, 2, 4, 6))
+    tok = dit.patchify(z, (1, 2, 2))
+    assert tok.shape == (2 * 2 * 3, 64)
+    # token (f=1, h'=1, w'=2) is index (1*2 + 1)*3 + 2 = 11; feature (c=5, i=1, j=0) = 5*4 + 2
+    assert tok[11, 5 * 4 + 2] == z[5, 1, 3, 4]
+    np.testing.assert_array_equal(dit.unpatchify(tok, z.shape, (1, 2, 2)), z)
+    z2 = RNG.standard_normal((16, 4, 4, 4))
+    tok2 = dit.patchify(z2, (2, 2, 2))
+    assert tok2[0, 3 * 8 + 1 * 4 + 1 * 2 + 0] == z2[3, 1, 1, 0]
+    np.testing.assert_array_equal(dit.unpatchify(tok2, z2.shape, (2, 2, 2)), z2)
+
+
+# --------------------------------------------------------------------------- blocks vs torch
+
+def T(a):
+    return torch.tensor(np.asarray(a, dtype=np.float64))
+
+
+def torch_rope(t, ang, n_video):
+    """t: [H, N, hd]; rotate video rows with complex multiplication."""
+    out = t.clone()
+    tv = t[:, :n_video].reshape(t.shape[0], n_video, -1, 2)
+    zc = torch.view_as_complex(tv.contiguous())
+    rot = torch.polar(torch.ones_like(T(ang)), T(ang))
+    out[:, :n_video] = torch.view_as_real(zc * rot).reshape(t.shape[0], n_video, -1)
+    return out
+
+
+def torch_attn(cfg, q, k, v, ang):
+    def heads(x):
+        return x.reshape(x.shape[0], cfg.heads, cfg.head_dim).transpose(0, 1)
+    q, k, v = heads(q), heads(k), heads(v)
+    q = tF.rms_norm(q, (cfg.head_dim,), eps=1e-6)
+    k = tF.rms_norm(k, (cfg.head_dim,), eps=1e-6)
+    q, k = torch_rope(q, ang, cfg.n_video), torch_rope(k, ang, cfg.n_video)
+    o = tF.scaled_dot_product_attention(q, k, v)
+    return o.transpose(0, 1).reshape(-1, cfg.hidden)
+
+
+def torch_block(W, cfg, b, x, c):
+    """Independent composition of a block from torch functional ops."""
+    d = cfg.hidden
+    x, c = T(x), T(c)
+    lin = lambda n, y: tF.linear(y, T(W[n + ".w"]), T(W[n + ".b"]))
+    ln = lambda y: tF.layer_norm(y, (d,), eps=1e-6)
+    ang = dit.rope_angles(cfg.grid, cfg.rope)
+    kind, pre = dit.block_kind(cfg, b), dit.block_prefix(cfg, b)
+    sc = tF.silu(c)
+    if kind == "seq":
+        m = lin(pre + ".ada", sc).chunk(6)
+        h = ln(x) * (1 + m[1]) + m[0]
+        q, k, v = lin(pre + ".qkv", h).chunk(3, dim=-1)
+        x = x + m[2] * lin(pre + ".out", torch_attn(cfg, q, k, v, ang))
+        h = ln(x) * (1 + m[4]) + m[3]
+        return (x + m[5] * lin(pre + ".fc2", tF.gelu(lin(pre + ".fc1", h), approximate="tanh"))).numpy()
+    if kind == "dual":
+        nv = cfg.n_video
+        mv, mt = lin(pre + ".vid.ada", sc).chunk(6), lin(pre + ".txt.ada", sc).chunk(6)
+        xv, xt = x[:nv], x[nv:]
+        qv, kv, vv = lin(pre + ".vid.qkv", ln(xv) * (1 + mv[1]) + mv[0]).chunk(3, dim=-1)
+        qt, kt, vt = lin(pre + ".txt.qkv", ln(xt) * (1 + mt[1]) + mt[0]).chunk(3, dim=-1)
+        o = torch_attn(cfg, torch.cat([qv, qt]), torch.cat([kv, kt]), torch.cat([vv, vt]), ang)
+        outs = []
+        for s, xs, ms, os_ in (("vid", xv, mv, o[:nv]), ("txt", xt, mt, o[nv:])):
+            xs = xs + ms[2] * lin(f"{pre}.{s}.out", os_)
+            h = ln(xs) * (1 + ms[4]) + ms[3]
+            outs.append(xs + ms[5] * lin(f"{pre}.{s}.fc2", tF.gelu(lin(f"{pre}.{s}.fc1", h), approximate="tanh")))
+        return torch.cat(outs).numpy()
+    m = lin(pre + ".ada", sc).chunk(3)
+    h = ln(x) * (1 + m[1]) + m[0]
+    y = lin(pre + ".lin1", h)
+    q, k, v, mm = y[:, :d], y[:, d:2 * d], y[:, 2 * d:3 * d], y[:, 3 * d:]
+    cat = torch.cat([torch_attn(cfg, q, k, v, ang), tF.gelu(mm, approximate="tanh")], dim=1)
+    return (x + m[2] * lin(pre + ".lin2", cat)).numpy()
+
+
+@pytest.mark.parametrize("block", [0, 1, 2])
+def test_blocks_match_torch_composition(block):
+    cfg = small_cfg()
+    W = {k: v.astype(np.float64) * 5 for k, v in synth.gen_weights(cfg).items()}   # larger weights: visible updates
+    x = RNG.standard_normal((cfg.n_tokens, cfg.hidden))
+    c = RNG.standard_normal(cfg.hidden)
+    got = dit.block_forward(W, cfg, block, x, c)
+    ref = torch_block(W, cfg, block, x, c)
+    assert np.abs(got - x).max() > 1e-2          # the block does something
+    np.testing.assert_allclose(got, ref, atol=1e-11)
+
+
+@pytest.mark.parametrize("block", [0, 1, 2])
+def test_block_rows_subset_equals_full(block):
+    cfg = small_cfg()
+    W = synth.gen_weights(cfg)
+    x = RNG.standard_normal((cfg.n_tokens, cfg.hidden))
+    c = RNG.standard_normal(cfg.hidden)
+    full = dit.block_forward(W, cfg, block, x, c)
+    rows = np.array([0, 5, cfg.n_video - 1, cfg.n_video, cfg.n_tokens - 1])
+    np.testing.assert_allclose(dit.block_forward(W, cfg, block, x, c, rows=rows), full[rows], atol=1e-13)
+
+
+@pytest.mark.parametrize("block", [0, 1, 2])
+def test_zero_gate_block_is_identity(block):
+    """adaLN with zero modulation weights and biases gives gates of 0: the block is the identity."""
+    cfg = small_cfg()
+    W = dict(synth.gen_weights(cfg))
+    for k in list(W):
+        if ".ada." in k:
+            W[k] = np.zeros_like(W[k])
+    x = RNG.standard_normal((cfg.n_tokens, cfg.hidden))
+    np.testing.assert_array_equal(dit.block_forward(W, cfg, block, x, RNG.standard_normal(cfg.hidden)), x)
+
+
+def test_attention_invariant_to_global_position_shift():
+    """With RoPE, shifting every video position by the same offset leaves scores unchanged."""
+    cfg = small_cfg()
+    ang = dit.rope_angles(cfg.grid, cfg.rope)
+    # angles for positions shifted by +1 along every axis
+    pos = dit.token_positions(cfg.grid).astype(float) + 1.0
+    parts = []
+    for a, d in enumerate(cfg.rope):
+        j = np.arange(d // 2)
+        parts.append(np.outer(pos[:, a], 10000.0 ** (-2.0 * j / d)))
+    ang2 = np.concatenate(parts, 1)
+    q, k, v = (RNG.standard_normal((2, cfg.n_video, cfg.head_dim)) for _ in range(3))
+    a1 = dit.attention(dit.apply_rope(q, ang), dit.apply_rope(k, ang), v)
+    a2 = dit.attention(dit.apply_rope(q, ang2), dit.apply_rope(k, ang2), v)
+    np.testing.assert_allclose(a1, a2, atol=1e-12)
+
+
+def test_forward_final_layer_and_conditioning():
+    cfg = small_cfg()
+    W = synth.gen_weights(cfg)
+    inp = synth.gen_inputs(cfg)
+    v = dit.dit_forward(W, cfg, inp["z_T"], 0.5, inp["cond"], inp["text"], inp["cam"])
+    assert v.shape == cfg.latent and np.all(np.isfinite(v))
+    # conditioning: timestep MLP plus linear condition and camera terms, by torch
+    c = tF.linear(tF.silu(tF.linear(T(dit.timestep_features(0.5)), T(W["t_embed.fc1.w"]), T(W["t_embed.fc1.b"]))),
+                  T(W["t_embed.fc2.w"]), T(W["t_embed.fc2.b"]))
+    c = c + tF.linear(T(inp["cond"]), T(W["cond_embed.w"]), T(W["cond_embed.b"]))
+    c = c + tF.linear(T(inp["cam"]), T(W["cam_embed.w"]), T(W["cam_embed.b"]))
+    np.testing.assert_allclose(dit.cond_embedding(W, cfg, 0.5, inp["cond"], inp["cam"]), c.numpy(), atol=1e-13)
+    # the output head only reads video tokens: changing text-token rows of the stream leaves v alone
+    x = dit.embed_tokens(W, cfg, inp["z_T"], inp["text"])
+    cemb = c.numpy()
+    v1 = dit.final_layer(W, cfg, x[: cfg.n_video], cemb)
+    x[cfg.n_video:] += 100
+    np.testing.assert_array_equal(dit.final_layer(W, cfg, x[: cfg.n_video], cemb), v1)
