@@ -1,0 +1,241 @@
+/*
+ * wdc.h -- C ABI of the WorldDynCache denoising-rollout library for MI355X (gfx950).
+ *
+ * The library runs the rollout of Eq. (1) of "WorldDynCache: Risk-Controlled
+ * Latent Dynamics Approximation for Diffusion World Models":
+ *     exact step      z_{t-1} = Psi_t(z_t, F_theta(z_t, t, c))
+ *     surrogate step  z_hat_{t-1} = G_t(z_t, H_t)
+ * with F_theta a synthetic video diffusion transformer (the paper does not fix
+ * its architecture), Psi_t the flow-matching Euler step, G_t the lifted latent
+ * surrogate of Eq. (2)-(5) and the choice between them made by the transition
+ * risk controller of Eq. (6)-(10).
+ *
+ * Conventions shared by every call
+ *  - Pointers prefixed d_ are device pointers, h_ host pointers. The caller owns
+ *    every buffer; the library borrows them for the duration of the call and
+ *    never frees them. Device buffers must be 16-byte aligned (E_ALIGN).
+ *  - Element types: float32, or bfloat16 passed as raw uint16 bit patterns
+ *    ("model dtype" = the dtype field of the model descriptor).
+ *  - Work is enqueued on the context's stream. Calls returning host-side
+ *    decisions (wdc_surrogate_step, wdc_risk_update, wdc_rollout) synchronise
+ *    that stream before they return; the others are asynchronous.
+ *  - Every call returns wdc_status; nothing throws across the ABI. After a
+ *    failure wdc_last_error() describes it. One context serves one host thread.
+ */
+#ifndef WDC_H_
+#define WDC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct wdc_ctx wdc_ctx;
+typedef struct wdc_state wdc_state;
+typedef void *wdc_stream; /* a hipStream_t; NULL = the null stream */
+
+typedef enum {
+  WDC_OK = 0,
+  WDC_E_ARG = 1,         /* null pointer or out-of-range argument */
+  WDC_E_SHAPE = 2,       /* sizes inconsistent with the model descriptor */
+  WDC_E_DTYPE = 3,       /* unsupported element type */
+  WDC_E_ALIGN = 4,       /* device pointer not 16-byte aligned */
+  WDC_E_WORKSPACE = 5,   /* workspace/weights not bound or too small */
+  WDC_E_STATE = 6,       /* call not valid in the current state */
+  WDC_E_HIP = 7,         /* a HIP runtime call failed */
+  WDC_E_NONFINITE = 8,   /* a non-finite value where a finite one is required */
+  WDC_E_UNSUPPORTED = 9  /* configuration the kernels do not cover */
+} wdc_status;
+
+enum { WDC_F32 = 0, WDC_BF16 = 1 };
+
+/* Rollout modes. RISK: Eq. (10) as written. FORCED: the decision of step k is
+ * h_forced[k] (1 = surrogate), still falling back to exact when the candidate is
+ * unsupported (Sec. 4.3, last sentence of "Reliability Decision"). ALL_EXACT:
+ * every step exact; candidates are still built and logged. */
+enum { WDC_MODE_RISK = 0, WDC_MODE_FORCED = 1, WDC_MODE_ALL_EXACT = 2 };
+
+/* Phases of wdc_risk_update. */
+enum { WDC_PRE_DECISION = 0, WDC_POST_EXACT = 1, WDC_POST_SURROGATE = 2 };
+
+/* Synthetic denoiser F_theta. The token grid is
+ * (lat_f/patch_t, lat_h/patch_h, lat_w/patch_w); video token n = (f*H'+h)*W'+w;
+ * text tokens follow the video tokens in the joint sequence. Blocks are
+ * numbered globally: n_seq sequential, then n_dual dual-stream, then
+ * n_single single-stream. rope_{t,h,w}: rotary dims per axis (sum = head_dim,
+ * all 0 = no RoPE). */
+typedef struct {
+  int32_t dtype;      /* WDC_F32 or WDC_BF16: weights, activations, cond/text/cam inputs */
+  int32_t hidden;     /* D */
+  int32_t heads;
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t mlp_ratio;  /* MLP width = mlp_ratio * D */
+  int32_t n_seq, n_dual, n_single;
+  int32_t cond_dim;   /* pooled condition length (0: none) */
+  int32_t cam_dim;    /* camera/geometry vector length (0: none) */
+  int32_t text_tokens, text_dim;
+  int32_t lat_c, lat_f, lat_h, lat_w;
+  int32_t patch_t, patch_h, patch_w;
+  int32_t rope_t, rope_h, rope_w;
+  int32_t qk_norm;    /* 1: per-head RMSNorm on q and k */
+} wdc_model_desc;
+
+/* Constants of the method. The paper fixes the anchor-age limit (six) and the
+ * cap of 2 on w_t; the rest are set in its supplementary material and are
+ * readings here (wdc_params_default fills them). */
+typedef struct {
+  int32_t bank_capacity;            /* M, FIFO capacity of the exact-transition bank (<= WDC_MAX_BANK) */
+  int32_t age_max, n_min, k_init, k_ref;
+  double theta_sim, theta_q;        /* compatibility thresholds of N_t (Eq. (3)) */
+  double tau_in, tau_obs, gamma_q;  /* temperatures and phase penalty (Eq. (3), (5)) */
+  double alpha_min, alpha_max, eps; /* Eq. (4) */
+  double eps_nu;                    /* RMS normalisation of Eq. (2) */
+  double w_z, w_age, w_phase, w_cam, w_depth; /* Eq. (6) */
+  double eta0, beta_d, eta_min, eta_max;      /* Eq. (8) */
+  double a_cam, a_depth, a_phase, lam, r0;    /* Eq. (9) */
+  double tau_risk;                            /* Eq. (10) */
+} wdc_params;
+
+#define WDC_MAX_BANK 8
+#define WDC_SUMMARY_DIM 256
+
+/* Per-step record of the controller (one per denoising step). */
+typedef struct {
+  int32_t k, exact, bank, support, finite, available, slot;
+  int32_t pad_;
+  double t, alpha;
+  double pi[WDC_MAX_BANK], kappa[WDC_MAX_BANK], sims_in[WDC_MAX_BANK]; /* slot order */
+  double d_z, d_age, d_phase, p, d_hat, w, r_cand, margin, sim_margin;
+  double d_cf, eta, R; /* d_cf is NaN when no supported counterfactual existed */
+} wdc_step_log;
+
+/* ---------------------------------------------------------------- context */
+
+/* Fill *p with the default constants. */
+void wdc_params_default(wdc_params *p);
+
+/* Create a context for one model on one stream (the current HIP device).
+ * desc may describe zero blocks (surrogate-only use). */
+wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_stream stream, wdc_ctx **out);
+wdc_status wdc_destroy(wdc_ctx *ctx);
+/* Message of the last failure on this context ("" if none). ctx may be NULL
+ * for failures of wdc_create. */
+const char *wdc_last_error(const wdc_ctx *ctx);
+
+/* Weights: one caller-allocated device blob of wdc_weights_bytes() bytes in the
+ * model dtype. Tensor i (0 <= i < wdc_weight_count) has a name such as
+ * "single.3.lin1.w", a shape (Linear weights are [out, in], biases [out]) and a
+ * byte offset inside the blob (256-byte aligned). */
+size_t wdc_weights_bytes(const wdc_ctx *ctx);
+int32_t wdc_weight_count(const wdc_ctx *ctx);
+wdc_status wdc_weight_info(const wdc_ctx *ctx, int32_t i, const char **name, int64_t shape[2], int32_t *ndim,
+                           size_t *offset);
+wdc_status wdc_bind_weights(wdc_ctx *ctx, const void *d_weights, size_t bytes);
+/* Fill a weights blob with N(0, std^2) values from a counter-based generator
+ * keyed by seed (throughput runs at sizes where host generation is too slow). */
+wdc_status wdc_init_weights_random(wdc_ctx *ctx, void *d_weights, size_t bytes, uint64_t seed, float std);
+
+/* Workspace for the denoiser and the rollout loop: caller-allocated device
+ * memory of wdc_workspace_bytes() bytes, bound once. */
+size_t wdc_workspace_bytes(const wdc_ctx *ctx);
+wdc_status wdc_bind_workspace(wdc_ctx *ctx, void *d_ws, size_t bytes);
+
+/* Rollout state: bank B_t (M exact output latents), anchor, history summary,
+ * risk R, eta_d and counters (Sec. 4.2-4.3). Its device memory
+ * (wdc_state_bytes) is caller-allocated; the state object itself is freed by
+ * wdc_state_destroy. h_cam: host float camera vector of cam_dim values for the
+ * lifted state's camera descriptor, or NULL (descriptor zero). */
+size_t wdc_state_bytes(const wdc_ctx *ctx);
+wdc_status wdc_state_create(wdc_ctx *ctx, void *d_mem, size_t bytes, wdc_state **out);
+wdc_status wdc_state_reset(wdc_state *st, const float *h_cam);
+wdc_status wdc_state_destroy(wdc_state *st);
+/* Bank introspection: device pointer of slot i's exact output latent, and the
+ * number of records inserted so far. */
+wdc_status wdc_state_bank_slot(wdc_state *st, int32_t i, float **d_slot, int32_t *inserts);
+
+/* ---------------------------------------------------------------- denoiser F_theta */
+
+/* c_emb = MLP(sinusoid(1000 t)) + Linear(cond) + Linear(cam): the conditioning
+ * vector every block modulates from. d_cond [cond_dim], d_cam [cam_dim] in the
+ * model dtype (NULL when the descriptor has none); d_cemb [D] float32 out. */
+wdc_status wdc_cond_embed(wdc_ctx *ctx, double t, const void *d_cond, const void *d_cam, float *d_cemb);
+
+/* One block (global index) of F_theta, in place on the joint residual stream.
+ * d_x: [N_video + text_tokens, D] float32, video rows first; d_cemb: [D] float32.
+ * Sequential blocks act on all rows with shared weights; dual-stream blocks
+ * use per-stream weights for the video and text rows and one joint attention;
+ * single-stream blocks use the fused linear1/linear2 form. */
+wdc_status wdc_dit_block_forward(wdc_ctx *ctx, int32_t block, float *d_x, const float *d_cemb);
+
+/* v = F_theta(z, t, c). d_z, d_v: [C, F, H, W] float32; d_cond/d_text/d_cam in
+ * the model dtype (text [text_tokens, text_dim]), NULL when absent. */
+wdc_status wdc_dit_forward(wdc_ctx *ctx, const float *d_z, double t, const void *d_cond, const void *d_text,
+                           const void *d_cam, float *d_v);
+
+/* ---------------------------------------------------------------- scheduler Psi_t */
+
+/* Flow-matching Euler step of Eq. (1): z_next = z + (t_next - t_cur) * v,
+ * numel float32 elements. d_z_next may equal d_z. */
+wdc_status wdc_scheduler_step(wdc_ctx *ctx, const float *d_z, const float *d_v, double t_cur, double t_next,
+                              float *d_z_next, int64_t numel);
+
+/* ---------------------------------------------------------------- surrogate and risk */
+
+/* Candidate of step k of an S-step rollout (t_k = (S-k)/S), Eq. (2)-(5):
+ * lifts d_z with the state's anchor and history, retrieves compatible records,
+ * evolves the lifted state and writes z_hat = sum_i kappa_i z_i^out into
+ * d_zhat [numel of the latent]. With an empty bank nothing is written. The
+ * candidate is kept in the state (d_zhat must stay valid until the matching
+ * wdc_risk_update) and described in *h_log (candidate fields). */
+wdc_status wdc_surrogate_step(wdc_ctx *ctx, wdc_state *st, const float *d_z, int32_t k, int32_t S, float *d_zhat,
+                              wdc_step_log *h_log);
+
+/* Transition risk controller, Eq. (6)-(10).
+ * PRE_DECISION (after wdc_surrogate_step of the same k): proxy p_k, weight w_k,
+ *   R_cand, availability and the decision; h_log->exact = 1 means Exact.
+ * POST_EXACT: d_z_cur = z_k, d_z_next = the exact z_{k+1}; computes the
+ *   counterfactual defect of the kept candidate (Eq. (7)), calibrates eta_d
+ *   (Eq. (8)) when that candidate was supported, decays R, inserts the record
+ *   (FIFO), moves the anchor to z_k and resets the surrogate count.
+ * POST_SURROGATE: R <- R_cand, one more consecutive surrogate step.
+ * Synchronises the stream. */
+wdc_status wdc_risk_update(wdc_ctx *ctx, wdc_state *st, int32_t phase, int32_t k, int32_t S, const float *d_z_cur,
+                           const float *d_z_next, wdc_step_log *h_log);
+
+/* The whole rollout of Sec. 4.4: S steps from d_z (in: z_T, out: z_0).
+ * mode: WDC_MODE_*; h_forced [S] (FORCED only); d_replay_v: NULL to evaluate
+ * F_theta, or [S, C, F, H, W] float32 velocities used at exact steps in place
+ * of F_theta. h_schedule [S] out: 0 = exact, 1 = surrogate; h_log [S] or NULL.
+ * The state is reset at the start (camera descriptor from d_cam). */
+wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const void *d_cond, const void *d_text,
+                       const void *d_cam, int32_t mode, const uint8_t *h_forced, const float *d_replay_v,
+                       uint8_t *h_schedule, wdc_step_log *h_log);
+
+/* ---------------------------------------------------------------- kernels exposed for tests and benchmarks */
+
+/* softmax(q k^T / sqrt(hd)) v over the full sequence, the attention of every
+ * block. d_q, d_k: [heads, n_pad, hd]; d_vt: [heads, hd, n_pad] (keys
+ * contiguous) for bf16, [heads, n_pad, hd] for float32; n valid tokens,
+ * n_pad = wdc_attn_pad(n); rows >= n of q/k/v must be zero. d_o: [n, ldo],
+ * head h written at columns [h*hd, (h+1)*hd). */
+int64_t wdc_attn_pad(int64_t n);
+wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
+                         int64_t ldo);
+
+/* c[m, n] = sum_k a[m, k] * w[n, k] + bias[n] in the model dtype with float32
+ * accumulation; a row stride lda, c row stride ldc. */
+wdc_status wdc_linear(wdc_ctx *ctx, const void *d_a, int64_t lda, const void *d_w, const void *d_bias, void *d_c,
+                      int64_t ldc, int64_t m, int64_t n, int64_t k);
+
+/* Seconds of GPU time of the last kernel of each class launched by this context
+ * when timing is on (wdc_set_timing(ctx, 1)); used by benchmarks. Index 0:
+ * attention, 1: GEMM, 2: everything else. */
+wdc_status wdc_set_timing(wdc_ctx *ctx, int32_t on);
+wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[3], int64_t out_count[3]);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WDC_H_ */

@@ -1,0 +1,308 @@
+// Attention of every denoiser block: O = softmax(Q K^T / sqrt(hd)) V over the
+// full (non-causal) spatio-temporal + text sequence.
+//
+// bf16 path (flash attention on the matrix cores, hd = 64 or 128):
+//  * each wavefront owns QT*32 queries; a 256-thread block owns 4*QT*32;
+//  * K tiles [64 keys][hd] and V^T tiles [hd][64 keys] are staged in LDS
+//    (double-buffered, next tile prefetched into registers);
+//  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the accumulator of a 32x32
+//    tile gives lane l one query (l % 32) and 16 keys, so the running max and
+//    sum of a query live in one lane and its partner l ^ 32 (one exchange);
+//  * O^T = V^T P^T reuses the S^T accumulators directly as the B operand: the
+//    8 accumulator values a lane holds for 16 consecutive keys become its 8
+//    bf16 k-values, and the V^T operand is read with the same key order, so P
+//    never goes through LDS;
+//  * online softmax in base 2 (scores pre-scaled by log2(e)/sqrt(hd)).
+// float32 path: a plain online-softmax kernel (tiny fp32 workload).
+#include "common.h"
+
+namespace wdc {
+
+int64_t attn_pad(int64_t n) { return ((n + 255) / 256) * 256; }
+
+namespace {
+
+// ---------------------------------------------------------------- float32 reference-style kernel
+// 16 queries per block, 16 threads per query, each thread owns hd/16 dims.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a) {
+  constexpr int PER = HD / 16;
+  constexpr int KT = 32;
+  __shared__ float Ks[KT][HD + 1];
+  __shared__ float Vs[KT][HD + 1];
+  const int h = blockIdx.y;
+  const int qi = threadIdx.x / 16, part = threadIdx.x % 16;
+  const int64_t q = (int64_t)blockIdx.x * 16 + qi;
+  const float *Q = (const float *)a.q + (int64_t)h * a.n_pad * HD;
+  const float *K = (const float *)a.k + (int64_t)h * a.n_pad * HD;
+  const float *V = (const float *)a.v + (int64_t)h * a.n_pad * HD;
+  const float scale = rsqrtf((float)HD);
+  float qv[PER], o[PER];
+  const int64_t qq = q < a.n ? q : 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    qv[i] = Q[qq * HD + part * PER + i] * scale;
+    o[i] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int64_t k0 = 0; k0 < a.n; k0 += KT) {
+    for (int i = threadIdx.x; i < KT * HD; i += 256) {
+      int r = i / HD, c = i % HD;
+      int64_t kr = k0 + r;
+      Ks[r][c] = kr < a.n ? K[kr * HD + c] : 0.f;
+      Vs[r][c] = kr < a.n ? V[kr * HD + c] : 0.f;
+    }
+    __syncthreads();
+    const int kn = (int)((a.n - k0) < KT ? (a.n - k0) : KT);
+    for (int j = 0; j < kn; ++j) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) s += qv[i] * Ks[j][part * PER + i];
+#pragma unroll
+      for (int o2 = 8; o2 > 0; o2 >>= 1) s += __shfl_xor(s, o2, 16);
+      float mn = fmaxf(m, s);
+      float al = expf(m - mn), p = expf(s - mn);
+      l = l * al + p;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) o[i] = o[i] * al + p * Vs[j][part * PER + i];
+      m = mn;
+    }
+    __syncthreads();
+  }
+  if (q < a.n) {
+    float *O = (float *)a.o + q * a.ldo + (int64_t)h * HD + part * PER;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) O[i] = o[i] / l;
+  }
+}
+
+// ---------------------------------------------------------------- bf16 flash attention on MFMA
+constexpr int KV = 64;  // keys per LDS tile
+
+template <int HD, int QT>
+struct ACfg {
+  static constexpr int NS = HD / 16;            // k-steps of S = K Q^T
+  static constexpr int NH = HD / 32;            // 32-row tiles of O^T along hd
+  static constexpr int QW = 32 * QT;            // queries per wave
+  static constexpr int QB = 4 * QW;             // queries per block
+  static constexpr int K_CHUNKS = KV * HD / 8 / 256;   // 16-byte chunks per thread per K tile
+  static constexpr int V_CHUNKS = HD * KV / 8 / 256;
+  static constexpr int K_ELEMS = KV * HD;
+  static constexpr int LDS_BYTES = 2 * 2 * KV * HD * 2;  // 2 buffers x (K + V^T)
+};
+
+// K tile: rows of HD bf16 = HD/8 16-byte chunks; chunk c of row r at c ^ (r & 7)
+template <int HD>
+__device__ __forceinline__ int kswz(int r, int c) { return r * HD + ((c ^ (r & 7)) << 3); }
+// V^T tile: rows of 64 bf16 = 16 8-byte chunks; chunk c of row r at c ^ (r & 15)
+__device__ __forceinline__ int vswz(int r, int c) { return r * KV + ((c ^ (r & 15)) << 2); }
+
+template <int HD, int QT>
+__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
+  using C = ACfg<HD, QT>;
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  bf16_t *sK = smem;                  // [2][KV][HD]
+  bf16_t *sV = smem + 2 * C::K_ELEMS; // [2][HD][KV]
+
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int64_t qbase = (int64_t)blockIdx.x * C::QB + wid * C::QW;
+  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
+  const bf16_t *K = (const bf16_t *)a.k + (int64_t)h * a.n_pad * HD;
+  const bf16_t *Vt = (const bf16_t *)a.v + (int64_t)h * HD * a.n_pad;
+
+  // Q^T as B operand: lane holds query qbase + 32*qt + lr, hd [16s + 8lg, +8)
+  bf16x8 qf[QT][C::NS];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s)
+      qf[qt][s] = *(const bf16x8 *)(Q + (qbase + 32 * qt + lr) * HD + 16 * s + 8 * lg);
+
+  uint4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
+  auto gload = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < C::K_CHUNKS; ++i) {
+      int idx = tid + i * 256;
+      int r = idx / (HD / 8), c = idx % (HD / 8);
+      rk[i] = *(const uint4 *)(K + (k0 + r) * HD + c * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < C::V_CHUNKS; ++i) {
+      int idx = tid + i * 256;
+      int r = idx / (KV / 8), c = idx % (KV / 8);
+      rv[i] = *(const uint4 *)(Vt + (int64_t)r * a.n_pad + k0 + c * 8);
+    }
+  };
+  auto sstore = [&](int buf) {
+    bf16_t *k = sK + buf * C::K_ELEMS, *v = sV + buf * C::K_ELEMS;
+#pragma unroll
+    for (int i = 0; i < C::K_CHUNKS; ++i) {
+      int idx = tid + i * 256;
+      int r = idx / (HD / 8), c = idx % (HD / 8);
+      *(uint4 *)(k + kswz<HD>(r, c)) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < C::V_CHUNKS; ++i) {
+      int idx = tid + i * 256;
+      int r = idx / (KV / 8), c = idx % (KV / 8);
+      *(uint2 *)(v + vswz(r, 2 * c)) = make_uint2(rv[i].x, rv[i].y);
+      *(uint2 *)(v + vswz(r, 2 * c + 1)) = make_uint2(rv[i].z, rv[i].w);
+    }
+  };
+
+  f32x16 o[C::NH][QT];
+#pragma unroll
+  for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][qt][e] = 0.f;
+  float m[QT], l[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m[qt] = -1e30f;
+    l[qt] = 0.f;
+  }
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+
+  const int ntiles = (int)((a.n + KV - 1) / KV);
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) gload((int64_t)(t + 1) * KV);
+    const bf16_t *k = sK + buf * C::K_ELEMS, *v = sV + buf * C::K_ELEMS;
+
+    // S^T = K Q^T: [2 key tiles][QT query tiles]
+    f32x16 s[2][QT];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[kt][qt][e] = 0.f;
+#pragma unroll
+    for (int st_ = 0; st_ < C::NS; ++st_) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        bf16x8 kf = *(const bf16x8 *)(k + kswz<HD>(32 * kt + lr, 2 * st_ + lg));
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+          s[kt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][st_], s[kt][qt], 0, 0, 0);
+      }
+    }
+    // key index of accumulator e of key tile kt: 32kt + 8(e/4) + 4lg + e%4
+    const int64_t k0 = (int64_t)t * KV;
+    const bool tail = k0 + KV > a.n;
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      float mx = m[qt];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float x = s[kt][qt][e] * sc;
+          if (tail) {
+            int64_t key = k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4);
+            if (key >= a.n) x = -1e30f;
+          }
+          s[kt][qt][e] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mx);
+      m[qt] = mx;
+      float sum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float p = __builtin_amdgcn_exp2f(s[kt][qt][e] - mx);
+          s[kt][qt][e] = p;
+          sum += p;
+        }
+      l[qt] = l[qt] * alpha + sum;
+#pragma unroll
+      for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
+    }
+    // O^T += V^T P^T over 4 k-steps of 16 keys
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      bf16x8 pf[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[qt][e] = (__bf16)s[j >> 1][qt][8 * (j & 1) + e];
+#pragma unroll
+      for (int i = 0; i < C::NH; ++i) {
+        const int r = 32 * i + lr;
+        uint2 lo = *(const uint2 *)(v + vswz(r, 4 * j + lg));
+        uint2 hi = *(const uint2 *)(v + vswz(r, 4 * j + 2 + lg));
+        uint4 pk = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        bf16x8 vf = *(bf16x8 *)&pk;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+          o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qt], o[i][qt], 0, 0, 0);
+      }
+    }
+    if (t + 1 < ntiles) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  // normalise and store: lane holds query 32qt + lr, hd 32i + 8(e/4) + 4lg + e%4
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);
+    const float inv = 1.f / lt;
+    const int64_t q = qbase + 32 * qt + lr;
+    if (q >= a.n) continue;
+    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+#pragma unroll
+    for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = 32 * i + 8 * g4 + 4 * lg;
+        uint32_t w0 = (uint32_t)f2bf(o[i][qt][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 1] * inv) << 16);
+        uint32_t w1 = (uint32_t)f2bf(o[i][qt][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 3] * inv) << 16);
+        *(uint2 *)(O + d0) = make_uint2(w0, w1);
+      }
+  }
+}
+
+template <int HD, int QT>
+hipError_t launch_bf16(const AttnArgs &a, hipStream_t s) {
+  using C = ACfg<HD, QT>;
+  static bool init = false;
+  if (!init) {
+    hipFuncSetAttribute((const void *)k_attn_bf16<HD, QT>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+    init = true;
+  }
+  dim3 grid((unsigned)((a.n + C::QB - 1) / C::QB), (unsigned)a.heads);
+  hipLaunchKernelGGL((k_attn_bf16<HD, QT>), grid, dim3(256), C::LDS_BYTES, s, a);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
+  if (dtype == 1) {
+    if (a.hd == 128) return launch_bf16<128, 1>(a, s);
+    if (a.hd == 64) return launch_bf16<64, 2>(a, s);
+    return hipErrorInvalidValue;
+  }
+  dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);
+  if (a.hd == 64)
+    hipLaunchKernelGGL(k_attn_f32<64>, grid, dim3(256), 0, s, a);
+  else if (a.hd == 128)
+    hipLaunchKernelGGL(k_attn_f32<128>, grid, dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace wdc

@@ -1,0 +1,407 @@
+// Memory-bound kernels of the denoiser: LayerNorm + adaLN modulation, q/k/v
+// preparation (per-head RMSNorm, 3D rotary embedding, attention layouts),
+// conditioning GEMVs, patch (un)folding and seeded initialisation.
+#include "common.h"
+
+namespace wdc {
+
+namespace {
+
+// ---------------------------------------------------------------- LayerNorm + modulate
+// One 256-thread block per row; the row stays in registers between the two
+// passes (mean, then variance of the centred values).
+template <typename T, int MAXV>
+__global__ __launch_bounds__(256) void k_ln_mod(const float *__restrict__ x, int64_t ldx, T *__restrict__ h,
+                                               int64_t ldh, int d, const float *__restrict__ shift,
+                                               const float *__restrict__ scale) {
+  __shared__ float red[8];
+  const int64_t r = blockIdx.x;
+  const float *xr = x + r * ldx;
+  float v[MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c = threadIdx.x + i * 256;
+    v[i] = c < d ? xr[c] : 0.f;
+    s += v[i];
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  s = warp_sum(s);
+  if (lane == 0) red[w] = s;
+  __syncthreads();
+  const float mean = (red[0] + red[1] + red[2] + red[3]) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c = threadIdx.x + i * 256;
+    float t = c < d ? v[i] - mean : 0.f;
+    q += t * t;
+  }
+  q = warp_sum(q);
+  if (lane == 0) red[4 + w] = q;
+  __syncthreads();
+  const float var = (red[4] + red[5] + red[6] + red[7]) / (float)d;
+  const float rstd = rsqrtf(var + 1e-6f);
+  T *hr = h + r * ldh;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c = threadIdx.x + i * 256;
+    if (c < d) st<T>(hr + c, (v[i] - mean) * rstd * (1.f + scale[c]) + shift[c]);
+  }
+}
+
+// ---------------------------------------------------------------- q/k preparation
+// One thread per rotary pair (2p, 2p+1) of one head of one row. The hd/2
+// threads of a head sit in one wavefront, so the RMS reduction is a shuffle.
+template <typename T, int HALF>
+__global__ __launch_bounds__(256) void k_qk_prep(QKVPrepArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int p = (int)(gid % HALF);
+  const int64_t rh = gid / HALF;
+  const int h = (int)(rh % a.heads);
+  const int64_t r = rh / a.heads;
+  const bool live = r < a.rows;
+  const int64_t rr = live ? r : 0;
+  const T *src = (const T *)a.src + rr * a.ld + (int64_t)h * a.hd + 2 * p;
+  float q0 = ld<T>(src), q1 = ld<T>(src + 1);
+  float k0 = ld<T>(src + a.d), k1 = ld<T>(src + a.d + 1);
+  if (a.qk_norm) {
+    float sq = q0 * q0 + q1 * q1, sk = k0 * k0 + k1 * k1;
+#pragma unroll
+    for (int o = HALF / 2; o > 0; o >>= 1) {
+      sq += __shfl_xor(sq, o, 64);
+      sk += __shfl_xor(sk, o, 64);
+    }
+    const float rq = rsqrtf(sq / (float)a.hd + 1e-6f), rk = rsqrtf(sk / (float)a.hd + 1e-6f);
+    q0 *= rq;
+    q1 *= rq;
+    k0 *= rk;
+    k1 *= rk;
+  }
+  const int64_t j = a.row0 + rr;  // joint-sequence index
+  if (a.rope && j < a.n_video) {
+    float2 cs = a.rope[j * HALF + p];
+    float t0 = q0 * cs.x - q1 * cs.y, t1 = q0 * cs.y + q1 * cs.x;
+    q0 = t0;
+    q1 = t1;
+    t0 = k0 * cs.x - k1 * cs.y;
+    t1 = k0 * cs.y + k1 * cs.x;
+    k0 = t0;
+    k1 = t1;
+  }
+  if (!live) return;
+  const int64_t o = ((int64_t)h * a.n_pad + j) * a.hd + 2 * p;
+  st<T>((T *)a.q + o, q0);
+  st<T>((T *)a.q + o + 1, q1);
+  st<T>((T *)a.k + o, k0);
+  st<T>((T *)a.k + o + 1, k1);
+}
+
+// v rows -> [H, n_pad, hd] (float32 attention path)
+template <typename T>
+__global__ __launch_bounds__(256) void k_v_copy(QKVPrepArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int c = (int)(gid % a.d);
+  const int64_t r = gid / a.d;
+  if (r >= a.rows) return;
+  const int h = c / a.hd, e = c % a.hd;
+  const T *src = (const T *)a.src + r * a.ld + 2 * a.d + c;
+  ((T *)a.v)[((int64_t)h * a.n_pad + a.row0 + r) * a.hd + e] = *src;
+}
+
+// v rows -> transposed [H, hd, n_pad] through a 64-row LDS tile, so that both
+// the reads (rows of the projection output) and the writes (runs of 64 tokens)
+// are coalesced.
+__global__ __launch_bounds__(256) void k_v_transpose(QKVPrepArgs a) {
+  __shared__ bf16_t tile[64][128 + 2];
+  const int h = blockIdx.y;
+  const int64_t r0 = (int64_t)blockIdx.x * 64;
+  for (int idx = threadIdx.x; idx < 64 * a.hd; idx += 256) {
+    int rr = idx / a.hd, e = idx % a.hd;
+    int64_t r = r0 + rr;
+    bf16_t val = 0;
+    if (r < a.rows) val = ((const bf16_t *)a.src)[r * a.ld + 2 * a.d + (int64_t)h * a.hd + e];
+    tile[rr][e] = val;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 64 * a.hd; idx += 256) {
+    int e = idx / 64, rr = idx % 64;
+    int64_t r = r0 + rr;
+    if (r < a.rows) ((bf16_t *)a.v)[((int64_t)h * a.hd + e) * a.n_pad + a.row0 + r] = tile[rr][e];
+  }
+}
+
+template <typename T>
+__global__ void k_qkv_pad(T *q, T *k, T *v, int heads, int hd, int64_t n, int64_t n_pad, int v_transposed) {
+  const int64_t tail = n_pad - n;
+  const int64_t total = (int64_t)heads * tail * hd;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    int e = (int)(i % hd);
+    int64_t rt = (i / hd) % tail;
+    int h = (int)(i / ((int64_t)hd * tail));
+    int64_t row = n + rt;
+    int64_t o = ((int64_t)h * n_pad + row) * hd + e;
+    q[o] = 0;
+    k[o] = 0;
+    if (v_transposed)
+      v[((int64_t)h * hd + e) * n_pad + row] = 0;
+    else
+      v[o] = 0;
+  }
+}
+
+// ---------------------------------------------------------------- GEMV (conditioning)
+// One wavefront per output row; 16-byte loads along the input dimension.
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemv(const T *__restrict__ w, const T *__restrict__ b,
+                                             const float *__restrict__ x, float *__restrict__ y, int n, int k,
+                                             int silu_in, int accumulate) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n) return;
+  const T *wr = w + (int64_t)row * k;
+  float acc = 0.f;
+  for (int j = lane; j < k; j += 64) {
+    float xv = x[j];
+    if (silu_in) xv = silu(xv);
+    acc += ld<T>(wr + j) * xv;
+  }
+  acc = warp_sum(acc);
+  if (lane == 0) {
+    float out = acc + (b ? ld<T>(b + row) : 0.f);
+    y[row] = accumulate ? y[row] + out : out;
+  }
+}
+
+// 16-byte vectorised bf16 variant for k % 512 == 0
+__global__ __launch_bounds__(256) void k_gemv_bf16_v(const bf16_t *__restrict__ w, const bf16_t *__restrict__ b,
+                                                    const float *__restrict__ x, float *__restrict__ y, int n, int k,
+                                                    int silu_in, int accumulate) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n) return;
+  const uint4 *wr = (const uint4 *)(w + (int64_t)row * k);
+  float acc = 0.f;
+  for (int j = lane; j < k / 8; j += 64) {
+    uint4 pk = wr[j];
+    const float *xp = x + j * 8;
+    uint32_t u[4] = {pk.x, pk.y, pk.z, pk.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float x0 = xp[2 * e], x1 = xp[2 * e + 1];
+      if (silu_in) {
+        x0 = silu(x0);
+        x1 = silu(x1);
+      }
+      acc += __uint_as_float(u[e] << 16) * x0 + __uint_as_float(u[e] & 0xffff0000u) * x1;
+    }
+  }
+  acc = warp_sum(acc);
+  if (lane == 0) {
+    float out = acc + (b ? bf2f(b[row]) : 0.f);
+    y[row] = accumulate ? y[row] + out : out;
+  }
+}
+
+__global__ void k_timestep(double t, float *out) {
+  int j = threadIdx.x;
+  if (j >= 128) return;
+  double f = exp(-log(10000.0) * (double)j / 128.0);
+  double arg = 1000.0 * t * f;
+  out[j] = (float)cos(arg);
+  out[128 + j] = (float)sin(arg);
+}
+
+template <typename T>
+__global__ void k_to_f32(const T *src, float *dst, int64_t n) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = ld<T>(src + i);
+}
+
+// ---------------------------------------------------------------- patches
+template <typename T>
+__global__ void k_patchify(const float *__restrict__ z, T *__restrict__ out, int c, int f, int h, int w, int pt,
+                           int ph, int pw) {
+  const int fp = f / pt, hp = h / ph, wp = w / pw;
+  const int P = c * pt * ph * pw;
+  const int64_t total = (int64_t)fp * hp * wp * P;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  int feat = (int)(i % P);
+  int64_t n = i / P;
+  int wq = (int)(n % wp), hq = (int)((n / wp) % hp), fq = (int)(n / ((int64_t)wp * hp));
+  int jj = feat % pw, ii = (feat / pw) % ph, aa = (feat / (pw * ph)) % pt, cc = feat / (pw * ph * pt);
+  int64_t src = (((int64_t)cc * f + (fq * pt + aa)) * h + (hq * ph + ii)) * w + (wq * pw + jj);
+  st<T>(out + i, z[src]);
+}
+
+__global__ void k_unpatchify(const float *__restrict__ tok, float *__restrict__ v, int c, int f, int h, int w, int pt,
+                             int ph, int pw) {
+  const int64_t total = (int64_t)c * f * h * w;
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= total) return;
+  int x = (int)(i % w), y = (int)((i / w) % h), fr = (int)((i / ((int64_t)w * h)) % f), cc = (int)(i / ((int64_t)w * h * f));
+  const int fp = f / pt, hp = h / ph, wp = w / pw;
+  (void)fp;
+  int64_t n = ((int64_t)(fr / pt) * hp + (y / ph)) * wp + (x / pw);
+  int feat = ((cc * pt + fr % pt) * ph + y % ph) * pw + x % pw;
+  v[i] = tok[n * (int64_t)(c * pt * ph * pw) + feat];
+}
+
+// ---------------------------------------------------------------- seeded normal fill
+// splitmix64 of (seed, counter) -> two 32-bit uniforms -> Box-Muller.
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  x += 0x9e3779b97f4a7c15ull;
+  x = (x ^ (x >> 30)) * 0xbf58476d1ce4e5b9ull;
+  x = (x ^ (x >> 27)) * 0x94d049bb133111ebull;
+  return x ^ (x >> 31);
+}
+
+template <typename T>
+__global__ void k_fill_normal(T *dst, int64_t n, uint64_t seed, uint64_t offset, float std) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) {
+    uint64_t r = splitmix64(seed * 0x632be59bd9b4e019ull + offset + (uint64_t)i);
+    float u1 = ((uint32_t)(r >> 32) + 1.0f) * 2.3283064365386963e-10f;  // (0, 1]
+    float u2 = (uint32_t)r * 2.3283064365386963e-10f;
+    float g = sqrtf(-2.f * logf(u1)) * cosf(6.283185307179586f * u2);
+    st<T>(dst + i, g * std);
+  }
+}
+
+__global__ void k_copy_rows(const float *src, int64_t lds, float *dst, int64_t ldd, int64_t rows, int64_t cols) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * cols) return;
+  int64_t r = i / cols, c = i % cols;
+  dst[r * ldd + c] = src[r * lds + c];
+}
+
+inline unsigned nblk(int64_t n, int t) { return (unsigned)((n + t - 1) / t); }
+}  // namespace
+
+hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, int64_t rows, int d,
+                         const float *shift, const float *scale, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d > 16 * 256) return hipErrorInvalidValue;
+  dim3 g((unsigned)rows), b(256);
+  if (dtype == 1) {
+    if (d <= 4 * 256)
+      hipLaunchKernelGGL((k_ln_mod<bf16_t, 4>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, d, shift, scale);
+    else
+      hipLaunchKernelGGL((k_ln_mod<bf16_t, 16>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, d, shift, scale);
+  } else {
+    if (d <= 4 * 256)
+      hipLaunchKernelGGL((k_ln_mod<float, 4>), g, b, 0, s, x, ldx, (float *)h, ldh, d, shift, scale);
+    else
+      hipLaunchKernelGGL((k_ln_mod<float, 16>), g, b, 0, s, x, ldx, (float *)h, ldh, d, shift, scale);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_prep(int dtype, const QKVPrepArgs &a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  if (a.hd != 64 && a.hd != 128) return hipErrorInvalidValue;
+  const int64_t threads = a.rows * a.heads * (a.hd / 2);
+  dim3 g(nblk(threads, 256)), b(256);
+  if (dtype == 1) {
+    if (a.hd == 64)
+      hipLaunchKernelGGL((k_qk_prep<bf16_t, 32>), g, b, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_qk_prep<bf16_t, 64>), g, b, 0, s, a);
+    hipLaunchKernelGGL(k_v_transpose, dim3(nblk(a.rows, 64), a.heads), dim3(256), 0, s, a);
+  } else {
+    if (a.hd == 64)
+      hipLaunchKernelGGL((k_qk_prep<float, 32>), g, b, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_qk_prep<float, 64>), g, b, 0, s, a);
+    hipLaunchKernelGGL((k_v_copy<float>), dim3(nblk(a.rows * a.d, 256)), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_pad(int dtype, void *q, void *k, void *v, int heads, int hd, int64_t n, int64_t n_pad,
+                          hipStream_t s) {
+  if (n_pad <= n) return hipSuccess;
+  int64_t total = (int64_t)heads * (n_pad - n) * hd;
+  unsigned g = nblk(total, 256);
+  if (g > 4096) g = 4096;
+  if (dtype == 1)
+    hipLaunchKernelGGL((k_qkv_pad<bf16_t>), dim3(g), dim3(256), 0, s, (bf16_t *)q, (bf16_t *)k, (bf16_t *)v, heads,
+                       hd, n, n_pad, 1);
+  else
+    hipLaunchKernelGGL((k_qkv_pad<float>), dim3(g), dim3(256), 0, s, (float *)q, (float *)k, (float *)v, heads, hd,
+                       n, n_pad, 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(int dtype, const void *w, const void *b, const float *x, float *y, int n, int k, int silu_in,
+                       int accumulate, hipStream_t s) {
+  dim3 g(nblk(n, 4)), bl(256);
+  if (dtype == 1) {
+    if (k % 512 == 0 && ((uintptr_t)w & 15) == 0)
+      hipLaunchKernelGGL(k_gemv_bf16_v, g, bl, 0, s, (const bf16_t *)w, (const bf16_t *)b, x, y, n, k, silu_in,
+                         accumulate);
+    else
+      hipLaunchKernelGGL((k_gemv<bf16_t>), g, bl, 0, s, (const bf16_t *)w, (const bf16_t *)b, x, y, n, k, silu_in,
+                         accumulate);
+  } else {
+    hipLaunchKernelGGL((k_gemv<float>), g, bl, 0, s, (const float *)w, (const float *)b, x, y, n, k, silu_in,
+                       accumulate);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_timestep_features(double t, float *out, hipStream_t s) {
+  hipLaunchKernelGGL(k_timestep, dim3(1), dim3(128), 0, s, t, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_to_f32(int dtype, const void *src, float *dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL((k_to_f32<bf16_t>), dim3(nblk(n, 256)), dim3(256), 0, s, (const bf16_t *)src, dst, n);
+  else
+    hipLaunchKernelGGL((k_to_f32<float>), dim3(nblk(n, 256)), dim3(256), 0, s, (const float *)src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_patchify(int dtype, const float *z, void *out, int c, int f, int h, int w, int pt, int ph, int pw,
+                           hipStream_t s) {
+  int64_t total = (int64_t)c * f * h * w;
+  if (dtype == 1)
+    hipLaunchKernelGGL((k_patchify<bf16_t>), dim3(nblk(total, 256)), dim3(256), 0, s, z, (bf16_t *)out, c, f, h, w,
+                       pt, ph, pw);
+  else
+    hipLaunchKernelGGL((k_patchify<float>), dim3(nblk(total, 256)), dim3(256), 0, s, z, (float *)out, c, f, h, w, pt,
+                       ph, pw);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpatchify(const float *tok, float *v, int c, int f, int h, int w, int pt, int ph, int pw,
+                             hipStream_t s) {
+  int64_t total = (int64_t)c * f * h * w;
+  hipLaunchKernelGGL(k_unpatchify, dim3(nblk(total, 256)), dim3(256), 0, s, tok, v, c, f, h, w, pt, ph, pw);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_normal(int dtype, void *dst, int64_t n, uint64_t seed, uint64_t offset, float std,
+                              hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  unsigned g = nblk(n, 256);
+  if (g > 65536) g = 65536;
+  if (dtype == 1)
+    hipLaunchKernelGGL((k_fill_normal<bf16_t>), dim3(g), dim3(256), 0, s, (bf16_t *)dst, n, seed, offset, std);
+  else
+    hipLaunchKernelGGL((k_fill_normal<float>), dim3(g), dim3(256), 0, s, (float *)dst, n, seed, offset, std);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows_f32(const float *src, int64_t lds, float *dst, int64_t ldd, int64_t rows, int64_t cols,
+                                hipStream_t s) {
+  if (rows * cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_rows, dim3(nblk(rows * cols, 256)), dim3(256), 0, s, src, lds, dst, ldd, rows, cols);
+  return hipGetLastError();
+}
+
+}  // namespace wdc

@@ -1,0 +1,243 @@
+// GEMMs of the denoiser: c[m, n] = sum_k a[m, k] * w[n, k] + bias[n] with a
+// fused epilogue (store, GELU-tanh, gated residual into the float32 stream,
+// float32 store). Both operands are K-contiguous ("NT"), which is the layout
+// the MFMA operand registers want: every lane loads 8 consecutive bf16.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 tiles, BMxBN block tile, BK = 64,
+// double-buffered LDS with an XOR swizzle of the 16-byte chunks of each
+// 128-byte row (conflict-free fragment reads), the next K tile prefetched into
+// registers while the current one feeds the matrix cores.
+// float32 path (tiny fp32 workload, and shapes the MFMA tiles do not cover):
+// a plain LDS-tiled FMA kernel.
+#include "common.h"
+
+namespace wdc {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ void epilogue(const GemmArgs &g, int epi, int64_t row, int64_t col, float acc) {
+  float v = acc + (g.bias ? ld<T>((const T *)g.bias + col) : 0.f);
+  int64_t o = row * g.ldc + col;
+  switch (epi) {
+    case EPI_STORE: st<T>((T *)g.c + o, v); break;
+    case EPI_GELU: st<T>((T *)g.c + o, gelu_tanh(v)); break;
+    case EPI_GATE_RES: ((float *)g.c)[o] += g.gate[col] * v; break;
+    default: ((float *)g.c)[o] = v; break;
+  }
+}
+
+// ---------------------------------------------------------------- generic tiled kernel
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const T *A = (const T *)g.a, *W = (const T *)g.w;
+  float acc[4][4] = {};
+  for (int64_t k0 = 0; k0 < g.k; k0 += 16) {
+    for (int i = threadIdx.x; i < 64 * 16; i += 256) {
+      int r = i / 16, kk = i % 16;
+      int64_t gr = m0 + r, gk = k0 + kk;
+      As[kk][r] = (gr < g.m && gk < g.k) ? ld<T>(A + gr * g.lda + gk) : 0.f;
+      int64_t gn = n0 + r;
+      Bs[kk][r] = (gn < g.n && gk < g.k) ? ld<T>(W + gn * g.k + gk) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = As[kk][ty * 4 + i];
+        b[i] = Bs[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int64_t r = m0 + ty * 4 + i, c = n0 + tx * 4 + j;
+      if (r < g.m && c < g.n) epilogue<T>(g, g.epi, r, c, acc[i][j]);
+    }
+}
+
+// ---------------------------------------------------------------- bf16 MFMA kernel
+constexpr int BK = 64;  // K per LDS stage: one 128-byte row of bf16 per tile row
+
+template <int BM, int BN, int WM, int WN>
+struct Cfg {
+  static constexpr int NT = 64 * WM * WN;       // threads
+  static constexpr int TM = BM / WM / 32;       // 32x32 tiles per wave along M
+  static constexpr int TN = BN / WN / 32;       // along N
+  static constexpr int A_CHUNKS = BM * 8 / NT;  // 16-byte chunks per thread per stage
+  static constexpr int B_CHUNKS = BN * 8 / NT;
+  static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
+};
+
+__device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chunk ^ (row & 7))) * 8; }
+
+template <int BM, int BN, int WM, int WN, int EPI>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
+  using C = Cfg<BM, BN, WM, WN>;
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  bf16_t *sA = smem;                      // [2][BM][64]
+  bf16_t *sB = smem + 2 * BM * BK;        // [2][BN][64]
+
+  // Tile order: a group of 8 consecutive M tiles walks all N tiles, so blocks
+  // running at once share A rows and the weight panel in L2.
+  const int n_tiles = (int)(g.n / BN);
+  const int m_tiles = (int)((g.m + BM - 1) / BM);
+  const int bid = blockIdx.x;
+  const int group = 8;
+  const int per_group = group * n_tiles;
+  const int gidx = bid / per_group;
+  const int first_m = gidx * group;
+  const int gsize = min(m_tiles - first_m, group);
+  const int mt = first_m + (bid % per_group) % gsize;
+  const int nt = (bid % per_group) / gsize;
+  const int64_t m0 = (int64_t)mt * BM, n0 = (int64_t)nt * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / WN, wn = wid % WN;
+  const bf16_t *A = (const bf16_t *)g.a, *W = (const bf16_t *)g.w;
+
+  // global -> register prefetch
+  uint4 ra[C::A_CHUNKS], rb[C::B_CHUNKS];
+  auto gload = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < C::A_CHUNKS; ++i) {
+      int idx = tid + i * C::NT;
+      int r = idx >> 3, ch = idx & 7;
+      int64_t gr = m0 + r;
+      gr = gr < g.m ? gr : g.m - 1;
+      ra[i] = *(const uint4 *)(A + gr * g.lda + k0 + ch * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_CHUNKS; ++i) {
+      int idx = tid + i * C::NT;
+      int r = idx >> 3, ch = idx & 7;
+      rb[i] = *(const uint4 *)(W + (n0 + r) * g.k + k0 + ch * 8);
+    }
+  };
+  auto sstore = [&](int buf) {
+    bf16_t *a = sA + buf * BM * BK, *b = sB + buf * BN * BK;
+#pragma unroll
+    for (int i = 0; i < C::A_CHUNKS; ++i) {
+      int idx = tid + i * C::NT;
+      *(uint4 *)(a + swz(idx >> 3, idx & 7)) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_CHUNKS; ++i) {
+      int idx = tid + i * C::NT;
+      *(uint4 *)(b + swz(idx >> 3, idx & 7)) = rb[i];
+    }
+  };
+
+  f32x16 acc[C::TM][C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = (int)(g.k / BK);
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int lr = lane & 31, lg = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((int64_t)(kt + 1) * BK);
+    const bf16_t *a = sA + buf * BM * BK, *b = sB + buf * BN * BK;
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      bf16x8 fa[C::TM], fb[C::TN];
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        int row = wm * (BM / WM) + i * 32 + lr;
+        fa[i] = *(const bf16x8 *)(a + swz(row, 2 * s + lg));
+      }
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        int row = wn * (BN / WN) + j * 32 + lr;
+        fb[j] = *(const bf16x8 *)(b + swz(row, 2 * s + lg));
+      }
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue: lane holds column lr of each 32x32 tile, rows 8*(e/4) + 4*lg + e%4
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t row = m0 + wm * (BM / WM) + i * 32 + 8 * (e / 4) + 4 * lg + (e % 4);
+        if (row < g.m) epilogue<bf16_t>(g, EPI, row, col, acc[i][j][e]);
+      }
+    }
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_mfma(const GemmArgs &g, hipStream_t s) {
+  using C = Cfg<BM, BN, WM, WN>;
+  const int m_tiles = (int)((g.m + BM - 1) / BM), n_tiles = (int)(g.n / BN);
+  dim3 grid(m_tiles * n_tiles), block(C::NT);
+  switch (g.epi) {
+    case EPI_STORE: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>), grid, block, C::LDS_BYTES, s, g); break;
+    case EPI_GELU: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>), grid, block, C::LDS_BYTES, s, g); break;
+    case EPI_GATE_RES: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>), grid, block, C::LDS_BYTES, s, g); break;
+    default: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>), grid, block, C::LDS_BYTES, s, g); break;
+  }
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN>
+void set_lds_limit() {
+  using C = Cfg<BM, BN, WM, WN>;
+  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+}
+}  // namespace
+
+hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
+  if (g.m <= 0 || g.n <= 0) return hipSuccess;
+  const bool aligned = ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0;
+  if (dtype == 1 && aligned) {
+    static bool init = false;
+    if (!init) {
+      set_lds_limit<256, 256, 2, 2>();
+      set_lds_limit<128, 128, 2, 2>();
+      init = true;
+    }
+    if (g.n % 256 == 0 && g.m >= 512) return launch_mfma<256, 256, 2, 2>(g, s);
+    if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
+  }
+  dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64)), block(256);
+  if (dtype == 1)
+    hipLaunchKernelGGL(k_gemm_simple<bf16_t>, grid, block, 0, s, g);
+  else
+    hipLaunchKernelGGL(k_gemm_simple<float>, grid, block, 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace wdc

@@ -1,0 +1,106 @@
+"""Kernel-level parity of the HIP path against the oracle (GPU)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import dit, scheduler
+from tests.gpu_util import TOL_F32, context, rel_l2, small_cfg, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def test_scheduler_step_matches_closed_form():
+    torch = torch_cuda()
+    ctx = context(synth.get_config("tiny"), weights=False)
+    rng = _rng(0)
+    for n in (1, 1000, 16 * 7 * 32 * 48 + 3):
+        z = rng.standard_normal(n).astype(np.float32)
+        v = rng.standard_normal(n).astype(np.float32)
+        zd, vd = (torch.from_numpy(a).cuda() for a in (z, v))
+        out = ctx.scheduler_step(zd, vd, 0.65, 0.6).cpu().numpy()
+        ref = scheduler.psi(z, v, 0.65, 0.6)
+        assert np.max(np.abs(out - ref)) <= 1e-6 * (1 + np.abs(ref).max())
+
+
+@pytest.mark.parametrize("dtype,m,n,k", [
+    ("bf16", 1000, 512, 3072), ("bf16", 600, 768, 1024), ("bf16", 300, 256, 128), ("bf16", 130, 384, 64),
+    ("bf16", 37, 64, 64), ("bf16", 1, 128, 256), ("f32", 300, 320, 96), ("f32", 5, 64, 256)])
+def test_linear_matches_oracle(dtype, m, n, k):
+    torch = torch_cuda()
+    cfg = synth.get_config("mid" if dtype == "bf16" else "tiny")
+    ctx = context(cfg, weights=False)
+    rng = _rng(m * 7 + n)
+    a = synth.stored(rng.standard_normal((m, k)), cfg.dtype)
+    w = synth.stored(rng.standard_normal((n, k)) * 0.05, cfg.dtype)
+    b = synth.stored(rng.standard_normal(n) * 0.1, cfg.dtype)
+    out = torch.empty((m, n), dtype=ctx.tdtype, device="cuda")
+    ctx.linear(ctx.to_device(a), ctx.to_device(w), ctx.to_device(b), out, m, n, k)
+    ref = dit.linear({"l.w": w, "l.b": b}, "l", a.astype(np.float64))
+    got = out.float().cpu().numpy()
+    err = rel_l2(got, ref)
+    # bf16: output rounding (2^-9) dominates; f32: accumulation order only
+    assert err <= (4e-3 if dtype == "bf16" else TOL_F32), err
+
+
+def _attn_inputs(ctx, heads, hd, n, seed, bf16):
+    torch = torch_cuda()
+    rng = _rng(seed)
+    q, k, v = (rng.standard_normal((heads, n, hd)) for _ in range(3))
+    if bf16:
+        q, k, v = (synth.round_bf16(x).astype(np.float64) for x in (q, k, v))
+    npad = ctx.attn_pad(n)
+    def pad(x):
+        out = np.zeros((heads, npad, hd), np.float32)
+        out[:, :n] = x
+        return out
+    qd, kd = ctx.to_device(pad(q)), ctx.to_device(pad(k))
+    vp = pad(v)
+    vd = ctx.to_device(np.ascontiguousarray(vp.transpose(0, 2, 1)) if bf16 else vp)
+    return (q, k, v), (qd, kd, vd)
+
+
+@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 700), (64, 61), (128, 512), (128, 1000), (128, 129)])
+def test_attention_bf16_matches_oracle(head_dim, n):
+    torch = torch_cuda()
+    cfg = small_cfg("bf16", head_dim=head_dim)
+    ctx = context(cfg, weights=False)
+    heads = cfg.heads
+    (q, k, v), (qd, kd, vd) = _attn_inputs(ctx, heads, head_dim, n, seed=n, bf16=True)
+    ldo = heads * head_dim + 32          # strided output rows
+    out = torch.zeros((n, ldo), dtype=torch.bfloat16, device="cuda")
+    ctx.attention(qd, kd, vd, n, out, ldo)
+    got = out.float().cpu().numpy()
+    ref = dit.attention(q, k, v).transpose(1, 0, 2).reshape(n, heads * head_dim)
+    err = rel_l2(got[:, : heads * head_dim], ref)
+    assert err <= 1e-2, err
+    assert np.all(got[:, heads * head_dim:] == 0)      # nothing written past the heads
+
+
+@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 77), (128, 100)])
+def test_attention_f32_matches_oracle(head_dim, n):
+    torch = torch_cuda()
+    cfg = small_cfg("f32", head_dim=head_dim)
+    ctx = context(cfg, weights=False)
+    (q, k, v), (qd, kd, vd) = _attn_inputs(ctx, cfg.heads, head_dim, n, seed=n + 1, bf16=False)
+    ldo = cfg.heads * head_dim
+    out = torch.zeros((n, ldo), dtype=torch.float32, device="cuda")
+    ctx.attention(qd, kd, vd, n, out, ldo)
+    ref = dit.attention(q, k, v).transpose(1, 0, 2).reshape(n, ldo)
+    assert rel_l2(out.cpu().numpy(), ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cond_embed_matches_oracle(dtype):
+    torch = torch_cuda()
+    cfg = small_cfg(dtype)
+    ctx = context(cfg)
+    W = synth.gen_weights(cfg)
+    inp = synth.gen_inputs(cfg)
+    for t in (1.0, 0.55, 0.0):
+        got = ctx.cond_embed(t, ctx.to_device(inp["cond"]), ctx.to_device(inp["cam"])).cpu().numpy()
+        ref = dit.cond_embedding(W, cfg, t, inp["cond"], inp["cam"])
+        assert rel_l2(got, ref) <= TOL_F32     # same (bf16-valued) weights, float32 accumulation
