@@ -77,7 +77,8 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------- bf16 flash attention on MFMA
-constexpr int KV = 64;  // keys per LDS tile
+constexpr int KV = 64;                   // keys per LDS tile
+constexpr int RSRC_WORD3 = 0x00020000;   // raw buffer descriptor word 3
 
 template <int HD, int QT>
 struct ACfg {
@@ -87,30 +88,29 @@ struct ACfg {
   static constexpr int QB = 4 * QW;             // queries per block
   static constexpr int K_CHUNKS = KV * HD / 8 / 256;   // 16-byte chunks per thread per K tile
   static constexpr int V_CHUNKS = HD * KV / 8 / 256;
-  static constexpr int K_ELEMS = KV * HD;
-  static constexpr int LDS_BYTES = 2 * 2 * KV * HD * 2;  // 2 buffers x (K + V^T)
+  static constexpr int K_BYTES = KV * HD * 2;
+  static constexpr int LDS_BYTES = 2 * 2 * K_BYTES;  // 2 buffers x (K + V^T)
 };
 
 // K tile: rows of HD bf16 = HD/8 16-byte chunks; chunk c of row r at c ^ (r & 7)
 template <int HD>
-__device__ __forceinline__ int kswz(int r, int c) { return r * HD + ((c ^ (r & 7)) << 3); }
+__device__ __forceinline__ int kswz(int r, int c) { return (r * (HD / 8) + (c ^ (r & 7))) * 16; }
 // V^T tile: rows of 64 bf16 = 16 8-byte chunks; chunk c of row r at c ^ (r & 15)
-__device__ __forceinline__ int vswz(int r, int c) { return r * KV + ((c ^ (r & 15)) << 2); }
+__device__ __forceinline__ int vswz(int r, int c) { return (r * 16 + (c ^ (r & 15))) * 8; }
 
 template <int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   using C = ACfg<HD, QT>;
-  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-  bf16_t *sK = smem;                  // [2][KV][HD]
-  bf16_t *sV = smem + 2 * C::K_ELEMS; // [2][HD][KV]
+  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char *sK = smem;                     // [2][KV][HD]
+  char *sV = smem + 2 * C::K_BYTES;    // [2][HD][KV]
 
   const int h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
   const int64_t qbase = (int64_t)blockIdx.x * C::QB + wid * C::QW;
   const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
-  const bf16_t *K = (const bf16_t *)a.k + (int64_t)h * a.n_pad * HD;
-  const bf16_t *Vt = (const bf16_t *)a.v + (int64_t)h * HD * a.n_pad;
 
   // Q^T as B operand: lane holds query qbase + 32*qt + lr, hd [16s + 8lg, +8)
   bf16x8 qf[QT][C::NS];
@@ -120,37 +120,23 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     for (int s = 0; s < C::NS; ++s)
       qf[qt][s] = *(const bf16x8 *)(Q + (qbase + 32 * qt + lr) * HD + 16 * s + 8 * lg);
 
-  uint4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
-  auto gload = [&](int64_t k0) {
-#pragma unroll
-    for (int i = 0; i < C::K_CHUNKS; ++i) {
-      int idx = tid + i * 256;
-      int r = idx / (HD / 8), c = idx % (HD / 8);
-      rk[i] = *(const uint4 *)(K + (k0 + r) * HD + c * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < C::V_CHUNKS; ++i) {
-      int idx = tid + i * 256;
-      int r = idx / (KV / 8), c = idx % (KV / 8);
-      rv[i] = *(const uint4 *)(Vt + (int64_t)r * a.n_pad + k0 + c * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-    bf16_t *k = sK + buf * C::K_ELEMS, *v = sV + buf * C::K_ELEMS;
-#pragma unroll
-    for (int i = 0; i < C::K_CHUNKS; ++i) {
-      int idx = tid + i * 256;
-      int r = idx / (HD / 8), c = idx % (HD / 8);
-      *(uint4 *)(k + kswz<HD>(r, c)) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::V_CHUNKS; ++i) {
-      int idx = tid + i * 256;
-      int r = idx / (KV / 8), c = idx % (KV / 8);
-      *(uint2 *)(v + vswz(r, 2 * c)) = make_uint2(rv[i].x, rv[i].y);
-      *(uint2 *)(v + vswz(r, 2 * c + 1)) = make_uint2(rv[i].z, rv[i].w);
-    }
-  };
+  // K rows and V^T rows of this head through buffer descriptors (byte offsets < 2^31)
+  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  // chunk i of this thread: K row tid/(HD/8) + i*(256/(HD/8)), chunk tid%(HD/8);
+  //                         V^T row tid/8 + 32 i, chunk tid%8
+  constexpr int KCPR = HD / 8, KROWS = 256 / KCPR;
+  const int kr = tid / KCPR, kc = tid % KCPR;
+  const int vr = tid >> 3, vc = tid & 7;
+  const int kvoff = kr * HD * 2 + kc * 16;
+  const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
+  const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
+  const int kst = kswz<HD>(kr, kc);            // same swizzle for every pass (KROWS % 8 == 0)
+  const int vst0 = vswz(vr, 2 * vc), vst1 = vswz(vr, 2 * vc + 1);
+
+  u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
 
   f32x16 o[C::NH][QT];
 #pragma unroll
@@ -165,16 +151,46 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     m[qt] = -1e30f;
     l[qt] = 0.f;
   }
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);   // log2(e)/sqrt(hd)
+
+  // fragment read offsets
+  int kro[C::NS];
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
+  int vro[4][2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    vro[j][0] = vswz(lr, 4 * j + lg);
+    vro[j][1] = vswz(lr, 4 * j + 2 + lg);
+  }
 
   const int ntiles = (int)((a.n + KV - 1) / KV);
-  gload(0);
-  sstore(0);
+#pragma unroll
+  for (int i = 0; i < C::K_CHUNKS; ++i) rk[i] = __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass, 0);
+#pragma unroll
+  for (int i = 0; i < C::V_CHUNKS; ++i) rv[i] = __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass, 0);
+#pragma unroll
+  for (int i = 0; i < C::K_CHUNKS; ++i) *(u32x4 *)(sK + kst + i * KROWS * HD * 2) = rk[i];
+#pragma unroll
+  for (int i = 0; i < C::V_CHUNKS; ++i) {
+    *(uint2 *)(sV + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);
+    *(uint2 *)(sV + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);
+  }
   __syncthreads();
+
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) gload((int64_t)(t + 1) * KV);
-    const bf16_t *k = sK + buf * C::K_ELEMS, *v = sV + buf * C::K_ELEMS;
+    const bool more = t + 1 < ntiles;
+    if (more) {
+      const int kb = (t + 1) * KV * HD * 2, vb = (t + 1) * KV * 2;
+#pragma unroll
+      for (int i = 0; i < C::K_CHUNKS; ++i)
+        rk[i] = __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass + kb, 0);
+#pragma unroll
+      for (int i = 0; i < C::V_CHUNKS; ++i)
+        rv[i] = __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass + vb, 0);
+    }
+    const char *k = sK + buf * C::K_BYTES, *v = sV + buf * C::K_BYTES;
 
     // S^T = K Q^T: [2 key tiles][QT query tiles]
     f32x16 s[2][QT];
@@ -188,47 +204,62 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     for (int st_ = 0; st_ < C::NS; ++st_) {
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        bf16x8 kf = *(const bf16x8 *)(k + kswz<HD>(32 * kt + lr, 2 * st_ + lg));
+        bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
           s[kt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][st_], s[kt][qt], 0, 0, 0);
       }
     }
-    // key index of accumulator e of key tile kt: 32kt + 8(e/4) + 4lg + e%4
+    // key of accumulator e of key tile kt: 32kt + 8(e/4) + 4lg + e%4
     const int64_t k0 = (int64_t)t * KV;
-    const bool tail = k0 + KV > a.n;
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      float mx = m[qt];
+    if (k0 + KV > a.n) {
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float x = s[kt][qt][e] * sc;
-          if (tail) {
-            int64_t key = k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4);
-            if (key >= a.n) x = -1e30f;
-          }
-          s[kt][qt][e] = x;
-          mx = fmaxf(mx, x);
-        }
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= a.n) s[kt][qt][e] = -1e30f;
+    }
+    bool moved = false;
+    float msc[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      float mx = s[0][qt][0];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mx);
-      m[qt] = mx;
+      const float mn = fmaxf(m[qt], mx * sc);   // running max of the scaled scores
+      moved |= mn > m[qt];
+      msc[qt] = mn;
+    }
+    // rescale the running sums and outputs only when some query's max moved
+    if (__any(moved)) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        const float alpha = __builtin_amdgcn_exp2f(m[qt] - msc[qt]);
+        l[qt] *= alpha;
+#pragma unroll
+        for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      m[qt] = msc[qt];
       float sum = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          float p = __builtin_amdgcn_exp2f(s[kt][qt][e] - mx);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][qt][e], sc, -msc[qt]));
           s[kt][qt][e] = p;
           sum += p;
         }
-      l[qt] = l[qt] * alpha + sum;
-#pragma unroll
-      for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
+      l[qt] += sum;
     }
     // O^T += V^T P^T over 4 k-steps of 16 keys
 #pragma unroll
@@ -240,17 +271,26 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         for (int e = 0; e < 8; ++e) pf[qt][e] = (__bf16)s[j >> 1][qt][8 * (j & 1) + e];
 #pragma unroll
       for (int i = 0; i < C::NH; ++i) {
-        const int r = 32 * i + lr;
-        uint2 lo = *(const uint2 *)(v + vswz(r, 4 * j + lg));
-        uint2 hi = *(const uint2 *)(v + vswz(r, 4 * j + 2 + lg));
-        uint4 pk = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        bf16x8 vf = *(bf16x8 *)&pk;
+        const char *vb = v + i * 32 * KV * 2;
+        const uint2 lo = *(const uint2 *)(vb + vro[j][0]);
+        const uint2 hi = *(const uint2 *)(vb + vro[j][1]);
+        u32x4 pk = {lo.x, lo.y, hi.x, hi.y};
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, pk);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
           o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qt], o[i][qt], 0, 0, 0);
       }
     }
-    if (t + 1 < ntiles) sstore(buf ^ 1);
+    if (more) {
+      char *nk = sK + (buf ^ 1) * C::K_BYTES, *nv = sV + (buf ^ 1) * C::K_BYTES;
+#pragma unroll
+      for (int i = 0; i < C::K_CHUNKS; ++i) *(u32x4 *)(nk + kst + i * KROWS * HD * 2) = rk[i];
+#pragma unroll
+      for (int i = 0; i < C::V_CHUNKS; ++i) {
+        *(uint2 *)(nv + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);
+        *(uint2 *)(nv + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);
+      }
+    }
     __syncthreads();
   }
   // normalise and store: lane holds query 32qt + lr, hd 32i + 8(e/4) + 4lg + e%4

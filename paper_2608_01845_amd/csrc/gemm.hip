@@ -11,6 +11,8 @@
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
 
+#include <cstdlib>
+
 namespace wdc {
 
 namespace {
@@ -71,6 +73,7 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g) {
 
 // ---------------------------------------------------------------- bf16 MFMA kernel
 constexpr int BK = 64;  // K per LDS stage: one 128-byte row of bf16 per tile row
+constexpr int RSRC_WORD3 = 0x00020000;  // raw buffer: 32-bit data format, no swizzle
 
 template <int BM, int BN, int WM, int WN>
 struct Cfg {
@@ -79,17 +82,29 @@ struct Cfg {
   static constexpr int TN = BN / WN / 32;       // along N
   static constexpr int A_CHUNKS = BM * 8 / NT;  // 16-byte chunks per thread per stage
   static constexpr int B_CHUNKS = BN * 8 / NT;
+  static constexpr int ROWS_PER_PASS = NT / 8;  // tile rows covered by one chunk index
   static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chunk ^ (row & 7))) * 8; }
+// Each tile row is 8 chunks of 16 bytes; chunk c of row r lives at c ^ (r & 7).
+__device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chunk ^ (row & 7))) * 16; }
+
+template <int EPI>
+__device__ __forceinline__ float epi_act(float v) {
+  if (EPI == EPI_GELU) {
+    // 0.5 v (1 + tanh(u)) = v * sigmoid(2u), u = sqrt(2/pi) (v + 0.044715 v^3)
+    const float u = 0.7978845608028654f * (v + 0.044715f * v * v * v);
+    return v / (1.f + __expf(-2.f * u));
+  }
+  return v;
+}
 
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
   using C = Cfg<BM, BN, WM, WN>;
-  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-  bf16_t *sA = smem;                      // [2][BM][64]
-  bf16_t *sB = smem + 2 * BM * BK;        // [2][BN][64]
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char *sA = smem;                      // [2][BM][128 B]
+  char *sB = smem + 2 * BM * BK * 2;    // [2][BN][128 B]
 
   // Tile order: a group of 8 consecutive M tiles walks all N tiles, so blocks
   // running at once share A rows and the weight panel in L2.
@@ -107,39 +122,31 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid / WN, wn = wid % WN;
-  const bf16_t *A = (const bf16_t *)g.a, *W = (const bf16_t *)g.w;
+  const int lr = lane & 31, lg = lane >> 5;
 
-  // global -> register prefetch
-  uint4 ra[C::A_CHUNKS], rb[C::B_CHUNKS];
-  auto gload = [&](int64_t k0) {
+  // buffer descriptors over this block's A rows and W rows; rows past m read as 0
+  const int64_t rows_a = min((int64_t)BM, g.m - m0);
+  const __amdgpu_buffer_rsrc_t ra_desc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)g.a + m0 * g.lda), (short)0, (int)(rows_a * g.lda * 2), RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t rb_desc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)g.w + n0 * g.k), (short)0, (int)(BN * g.k * 2), RSRC_WORD3);
+  const int crow = tid >> 3, cch = tid & 7;
+  const int va = crow * (int)g.lda * 2 + cch * 16;     // byte offset of this thread's chunk (pass 0)
+  const int vb = crow * (int)g.k * 2 + cch * 16;
+  const int pass_a = C::ROWS_PER_PASS * (int)g.lda * 2;
+  const int pass_b = C::ROWS_PER_PASS * (int)g.k * 2;
+  const int st_off = swz(crow, cch);                    // LDS byte offset of pass 0 (same swizzle every pass)
+
+  // fragment read offsets: row wm*(BM/WM) + 32i + lr, chunk 2s + lg (swizzle depends on lr only)
+  int ra_off[4], rb_off[4];
 #pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      int idx = tid + i * C::NT;
-      int r = idx >> 3, ch = idx & 7;
-      int64_t gr = m0 + r;
-      gr = gr < g.m ? gr : g.m - 1;
-      ra[i] = *(const uint4 *)(A + gr * g.lda + k0 + ch * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      int idx = tid + i * C::NT;
-      int r = idx >> 3, ch = idx & 7;
-      rb[i] = *(const uint4 *)(W + (n0 + r) * g.k + k0 + ch * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-    bf16_t *a = sA + buf * BM * BK, *b = sB + buf * BN * BK;
-#pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      int idx = tid + i * C::NT;
-      *(uint4 *)(a + swz(idx >> 3, idx & 7)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      int idx = tid + i * C::NT;
-      *(uint4 *)(b + swz(idx >> 3, idx & 7)) = rb[i];
-    }
-  };
+  for (int s = 0; s < 4; ++s) {
+    ra_off[s] = swz(wm * (BM / WM) + lr, 2 * s + lg);
+    rb_off[s] = swz(wn * (BN / WN) + lr, 2 * s + lg);
+  }
+
+  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+  u32x4 ra[C::A_CHUNKS], rb[C::B_CHUNKS];
 
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
@@ -150,49 +157,77 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int nk = (int)(g.k / BK);
-  gload(0);
-  sstore(0);
+  // prologue: tile 0
+#pragma unroll
+  for (int i = 0; i < C::A_CHUNKS; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(ra_desc, va, i * pass_a, 0);
+#pragma unroll
+  for (int i = 0; i < C::B_CHUNKS; ++i) rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb_desc, vb, i * pass_b, 0);
+#pragma unroll
+  for (int i = 0; i < C::A_CHUNKS; ++i) *(u32x4 *)(sA + st_off + i * C::ROWS_PER_PASS * 128) = ra[i];
+#pragma unroll
+  for (int i = 0; i < C::B_CHUNKS; ++i) *(u32x4 *)(sB + st_off + i * C::ROWS_PER_PASS * 128) = rb[i];
   __syncthreads();
-  const int lr = lane & 31, lg = lane >> 5;
+
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((int64_t)(kt + 1) * BK);
-    const bf16_t *a = sA + buf * BM * BK, *b = sB + buf * BN * BK;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int kb = (kt + 1) * BK * 2;
+#pragma unroll
+      for (int i = 0; i < C::A_CHUNKS; ++i)
+        ra[i] = __builtin_amdgcn_raw_buffer_load_b128(ra_desc, va, i * pass_a + kb, 0);
+#pragma unroll
+      for (int i = 0; i < C::B_CHUNKS; ++i)
+        rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb_desc, vb, i * pass_b + kb, 0);
+    }
+    const char *a = sA + buf * BM * 128, *b = sB + buf * BN * 128;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
       bf16x8 fa[C::TM], fb[C::TN];
 #pragma unroll
-      for (int i = 0; i < C::TM; ++i) {
-        int row = wm * (BM / WM) + i * 32 + lr;
-        fa[i] = *(const bf16x8 *)(a + swz(row, 2 * s + lg));
-      }
+      for (int i = 0; i < C::TM; ++i) fa[i] = *(const bf16x8 *)(a + ra_off[s] + i * 32 * 128);
 #pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        int row = wn * (BN / WN) + j * 32 + lr;
-        fb[j] = *(const bf16x8 *)(b + swz(row, 2 * s + lg));
-      }
+      for (int j = 0; j < C::TN; ++j) fb[j] = *(const bf16x8 *)(b + rb_off[s] + j * 32 * 128);
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+    if (more) {
+      char *na = sA + (buf ^ 1) * BM * 128, *nb = sB + (buf ^ 1) * BN * 128;
+#pragma unroll
+      for (int i = 0; i < C::A_CHUNKS; ++i) *(u32x4 *)(na + st_off + i * C::ROWS_PER_PASS * 128) = ra[i];
+#pragma unroll
+      for (int i = 0; i < C::B_CHUNKS; ++i) *(u32x4 *)(nb + st_off + i * C::ROWS_PER_PASS * 128) = rb[i];
+    }
     __syncthreads();
   }
 
   // epilogue: lane holds column lr of each 32x32 tile, rows 8*(e/4) + 4*lg + e%4
+  const bf16_t *bias = (const bf16_t *)g.bias;
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i)
+  for (int j = 0; j < C::TN; ++j) {
+    const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
+    const float bv = bias ? bf2f(bias[col]) : 0.f;
+    const float gv = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j) {
-      const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
+    for (int i = 0; i < C::TM; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t row = m0 + wm * (BM / WM) + i * 32 + 8 * (e / 4) + 4 * lg + (e % 4);
-        if (row < g.m) epilogue<bf16_t>(g, EPI, row, col, acc[i][j][e]);
+        if (row >= g.m) continue;
+        const float v = acc[i][j][e] + bv;
+        const int64_t o = row * g.ldc + col;
+        if (EPI == EPI_STORE || EPI == EPI_GELU)
+          ((bf16_t *)g.c)[o] = f2bf(epi_act<EPI>(v));
+        else if (EPI == EPI_GATE_RES)
+          ((float *)g.c)[o] += gv * v;
+        else
+          ((float *)g.c)[o] = v;
       }
     }
+  }
 }
 
 template <int BM, int BN, int WM, int WN>
@@ -226,10 +261,13 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
     static bool init = false;
     if (!init) {
       set_lds_limit<256, 256, 2, 2>();
+      set_lds_limit<256, 256, 2, 4>();
       set_lds_limit<128, 128, 2, 2>();
       init = true;
     }
-    if (g.n % 256 == 0 && g.m >= 512) return launch_mfma<256, 256, 2, 2>(g, s);
+    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
+    if (g.n % 256 == 0 && g.m >= 512)
+      return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s) : launch_mfma<256, 256, 2, 4>(g, s);
     if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
   }
   dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64)), block(256);
