@@ -16,6 +16,8 @@
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
+#include <cstdlib>
+
 namespace wdc {
 
 int64_t attn_pad(int64_t n) { return ((n + 255) / 256) * 256; }
@@ -313,6 +315,236 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   }
 }
 
+// Software-pipelined variant: K is staged one tile ahead of V, so S for tile
+// t+1 is issued on the matrix cores before the softmax of tile t runs on the
+// vector ALUs. LDS holds two K tiles and two V^T tiles:
+//   iteration t reads K_{t+1} (kbuf[(t+1)&1]) and V_t (vbuf[t&1]) and writes
+//   K_{t+2} into kbuf[t&1] (last read in iteration t-1) and V_{t+1} into
+//   vbuf[(t+1)&1] (last read in iteration t-1); one barrier per iteration.
+template <int HD, int QT, int MINB>
+__global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
+  using C = ACfg<HD, QT>;
+  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char *sK = smem;                     // [2][KV][HD]
+  char *sV = smem + 2 * C::K_BYTES;    // [2][HD][KV]
+
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int64_t qbase = (int64_t)blockIdx.x * C::QB + wid * C::QW;
+  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
+
+  bf16x8 qf[QT][C::NS];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s)
+      qf[qt][s] = *(const bf16x8 *)(Q + (qbase + 32 * qt + lr) * HD + 16 * s + 8 * lg);
+
+  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  constexpr int KCPR = HD / 8, KROWS = 256 / KCPR;
+  const int kr = tid / KCPR, kc = tid % KCPR;
+  const int vr = tid >> 3, vc = tid & 7;
+  const int kvoff = kr * HD * 2 + kc * 16;
+  const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
+  const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
+  const int kst = kswz<HD>(kr, kc);
+  const int vst0 = vswz(vr, 2 * vc), vst1 = vswz(vr, 2 * vc + 1);
+  int kro[C::NS];
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
+  int vro[4][2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    vro[j][0] = vswz(lr, 4 * j + lg);
+    vro[j][1] = vswz(lr, 4 * j + 2 + lg);
+  }
+
+  u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
+  const int ntiles = (int)((a.n + KV - 1) / KV);
+
+#define WDC_LOAD_K(tile)                                                                          \
+  _Pragma("unroll") for (int i = 0; i < C::K_CHUNKS; ++i) rk[i] =                                 \
+      __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass + (tile) * KV * HD * 2, 0)
+#define WDC_LOAD_V(tile)                                                                          \
+  _Pragma("unroll") for (int i = 0; i < C::V_CHUNKS; ++i) rv[i] =                                 \
+      __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass + (tile) * KV * 2, 0)
+#define WDC_STORE_K(b)                                                                            \
+  _Pragma("unroll") for (int i = 0; i < C::K_CHUNKS; ++i)                                         \
+      *(u32x4 *)(sK + (b) * C::K_BYTES + kst + i * KROWS * HD * 2) = rk[i]
+#define WDC_STORE_V(b)                                                                            \
+  _Pragma("unroll") for (int i = 0; i < C::V_CHUNKS; ++i) {                                       \
+    *(uint2 *)(sV + (b) * C::K_BYTES + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);     \
+    *(uint2 *)(sV + (b) * C::K_BYTES + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);     \
+  }
+
+  // prologue: K_0, V_0, K_1
+  WDC_LOAD_K(0);
+  WDC_LOAD_V(0);
+  WDC_STORE_K(0);
+  WDC_STORE_V(0);
+  if (ntiles > 1) {
+    WDC_LOAD_K(1);
+    WDC_STORE_K(1);
+  }
+  __syncthreads();
+
+  f32x16 o[C::NH][QT];
+#pragma unroll
+  for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][qt][e] = 0.f;
+  float m[QT], l[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m[qt] = -1e30f;
+    l[qt] = 0.f;
+  }
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+
+  f32x16 s[2][QT];
+  auto qk = [&](f32x16(&dst)[2][QT], const char *k) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) dst[kt][qt][e] = 0.f;
+#pragma unroll
+    for (int st_ = 0; st_ < C::NS; ++st_)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+          dst[kt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][st_], dst[kt][qt], 0, 0, 0);
+      }
+  };
+  qk(s, sK);
+
+  for (int t = 0; t < ntiles; ++t) {
+    const bool more_k = t + 2 < ntiles, more_v = t + 1 < ntiles;
+    if (more_k) WDC_LOAD_K(t + 2);
+    if (more_v) WDC_LOAD_V(t + 1);
+    f32x16 sn[2][QT];
+    if (more_v) qk(sn, sK + ((t + 1) & 1) * C::K_BYTES);
+
+    const int64_t k0 = (int64_t)t * KV;
+    if (k0 + KV > a.n) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= a.n) s[kt][qt][e] = -1e30f;
+    }
+    bool moved = false;
+    float msc[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      float mx = s[0][qt][0];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(m[qt], mx * sc);
+      moved |= mn > m[qt];
+      msc[qt] = mn;
+    }
+    if (__any(moved)) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        const float alpha = __builtin_amdgcn_exp2f(m[qt] - msc[qt]);
+        l[qt] *= alpha;
+#pragma unroll
+        for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
+      }
+    }
+    bf16x8 pf[4][QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      m[qt] = msc[qt];
+      float sum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][qt][e], sc, -msc[qt]));
+          sum += p;
+          pf[2 * kt + e / 8][qt][e % 8] = (__bf16)p;
+        }
+      l[qt] += sum;
+    }
+    const char *v = sV + (t & 1) * C::K_BYTES;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+      for (int i = 0; i < C::NH; ++i) {
+        const char *vb = v + i * 32 * KV * 2;
+        const uint2 lo = *(const uint2 *)(vb + vro[j][0]);
+        const uint2 hi = *(const uint2 *)(vb + vro[j][1]);
+        u32x4 pk = {lo.x, lo.y, hi.x, hi.y};
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, pk);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+          o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][qt], o[i][qt], 0, 0, 0);
+      }
+    }
+    if (more_k) WDC_STORE_K(t & 1);
+    if (more_v) WDC_STORE_V((t + 1) & 1);
+    __syncthreads();
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) s[kt][qt] = sn[kt][qt];
+  }
+#undef WDC_LOAD_K
+#undef WDC_LOAD_V
+#undef WDC_STORE_K
+#undef WDC_STORE_V
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);
+    const float inv = 1.f / lt;
+    const int64_t q = qbase + 32 * qt + lr;
+    if (q >= a.n) continue;
+    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+#pragma unroll
+    for (int i = 0; i < C::NH; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = 32 * i + 8 * g4 + 4 * lg;
+        uint32_t w0 = (uint32_t)f2bf(o[i][qt][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 1] * inv) << 16);
+        uint32_t w1 = (uint32_t)f2bf(o[i][qt][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 3] * inv) << 16);
+        *(uint2 *)(O + d0) = make_uint2(w0, w1);
+      }
+  }
+}
+
+template <int HD, int QT, int MINB>
+hipError_t launch_bf16_pipe(const AttnArgs &a, hipStream_t s) {
+  using C = ACfg<HD, QT>;
+  static bool init = false;
+  if (!init) {
+    hipFuncSetAttribute((const void *)k_attn_bf16_pipe<HD, QT, MINB>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                        C::LDS_BYTES);
+    init = true;
+  }
+  dim3 grid((unsigned)((a.n + C::QB - 1) / C::QB), (unsigned)a.heads);
+  hipLaunchKernelGGL((k_attn_bf16_pipe<HD, QT, MINB>), grid, dim3(256), C::LDS_BYTES, s, a);
+  return hipGetLastError();
+}
+
 template <int HD, int QT>
 hipError_t launch_bf16(const AttnArgs &a, hipStream_t s) {
   using C = ACfg<HD, QT>;
@@ -331,8 +563,18 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    if (a.hd == 128) return launch_bf16<128, 1>(a, s);
-    if (a.hd == 64) return launch_bf16<64, 2>(a, s);
+    // hd = 128: software-pipelined kernel, two blocks per CU; hd = 64: plain kernel
+    // (both measured fastest at the workload shapes). WDC_ATTN_VARIANT overrides.
+    static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : -1;
+    if (a.hd == 128) {
+      if (variant == 0) return launch_bf16<128, 1>(a, s);
+      if (variant == 1) return launch_bf16_pipe<128, 1, 1>(a, s);
+      return launch_bf16_pipe<128, 1, 2>(a, s);
+    }
+    if (a.hd == 64) {
+      if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(a, s);
+      return launch_bf16<64, 2>(a, s);
+    }
     return hipErrorInvalidValue;
   }
   dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);
