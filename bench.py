@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--workload", default="13b", choices=["13b", "5b", "mid", "tiny"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
     ap.add_argument("--surrogate-steps", type=int, default=20)
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="also run one plain device copy of this many bytes (hardware-counter calibration)")
     return ap.parse_args()
 
 
@@ -196,6 +198,14 @@ def main():
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
                      "traffic": None},
     }
+    if args.copy_probe > 0:
+        src = torch.empty(args.copy_probe // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_probe_bytes"] = args.copy_probe
+        del src, dst
     if not args.no_cpu:
         log("CPU oracle baseline ...")
         out["cpu_baseline"] = cpu_baseline(cfg)

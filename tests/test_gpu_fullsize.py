@@ -1,0 +1,92 @@
+"""Parity at the full workload sizes, in the kernels and launch shapes the
+benchmark times: every token goes through the GPU block; the oracle evaluates
+sampled output rows one by one (keys/values of all tokens, everything else for
+the sampled rows). Also the surrogate/risk kernels standalone on the largest
+latent (16 x 33 x 90 x 160)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import dit
+from oracle import params as P
+from oracle import rollout as ro
+from tests.gpu_util import TOL_BF16_BLOCK, TOL_F32, rel_l2, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_rows(cfg, n_random=40, seed=0):
+    n, nv = cfg.n_tokens, cfg.n_video
+    fixed = [0, 1, 63, 64, 127, 128, 255, 256, nv - 1, n - 1]
+    if cfg.text_tokens:
+        fixed += [nv, nv + 1]
+    rng = np.random.default_rng(seed)
+    rnd = rng.choice(n, size=n_random, replace=False)
+    return np.unique(np.concatenate([fixed, rnd])).astype(np.int64)
+
+
+def block_case(name, block):
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config(name)
+    pre = synth.block_prefix(cfg, block)
+    W = synth.gen_weights(cfg, names=[pre])
+    ctx = wdc.Context(cfg)
+    assert ctx.load_weights(W, strict=False) == len(W)
+    x = synth.gen_block_input(cfg)
+    c = synth.gen_cemb(cfg)
+    xd = torch.from_numpy(x).cuda()
+    ctx.block_forward(block, xd, torch.from_numpy(c).cuda())
+    rows = sample_rows(cfg)
+    got = xd[torch.from_numpy(rows).cuda()].cpu().numpy()
+    del xd, ctx
+    torch.cuda.empty_cache()
+    ref = dit.block_forward(W, cfg, block, x, c, rows=rows)
+    err, derr = rel_l2(got, ref), rel_l2(got - x[rows], ref - x[rows])
+    print(f"{name} block {block} ({dit.block_kind(cfg, block)}), {len(rows)} rows of {cfg.n_tokens}: "
+          f"rel_l2 {err:.2e}, update rel_l2 {derr:.2e}")
+    assert np.all(np.isfinite(got))
+    assert err <= TOL_BF16_BLOCK and derr <= 5e-2
+
+
+def test_13b_dual_block_sampled_rows():
+    block_case("13b", 0)
+
+
+def test_13b_single_block_sampled_rows():
+    block_case("13b", 59)
+
+
+def test_5b_joint_block_sampled_rows():
+    block_case("5b", 7)
+
+
+def test_stress_single_block_118800_tokens_sampled_rows():
+    block_case("stress", 0)
+
+
+def test_stress_surrogate_and_risk_on_largest_latent():
+    """Forced schedule over 8 steps with recorded velocities on the 16x33x90x160
+    latent: 4 exact inserts fill the bank, surrogate steps read all 4 records."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config("stress")
+    steps = 8
+    mask = [0, 1, 0, 0, 1, 0, 1, 1]
+    vel = synth.gen_replay_velocities(cfg, steps)
+    z0 = synth.gen_inputs(cfg)["z_T"]
+    ref = ro.rollout(ro.replay_denoiser(vel), z0, steps, P.DEFAULTS, mode="forced", forced=mask)
+    ctx = wdc.Context(cfg, allocate_weights=False)
+    z = torch.from_numpy(z0).cuda()
+    sched, logs = ctx.rollout(ctx.new_state(), z, steps, mode=wdc.MODE_FORCED, forced=mask,
+                              replay_v=torch.from_numpy(vel).cuda())
+    assert sched == ref.schedule
+    for g, o in zip(logs, ref.log):
+        assert g["exact"] == int(o.exact) and g["support"] == o.support and g["bank"] == o.bank
+        np.testing.assert_allclose(g["kappa"], o.kappa, atol=1e-6)
+        for key in ("d_z", "p", "r_cand", "eta", "R"):
+            assert abs(g[key] - getattr(o, key)) <= 1e-5 * max(1.0, abs(getattr(o, key))), key
+        if o.exact and np.isfinite(o.d_cf):
+            assert abs(g["d_cf"] - o.d_cf) <= 1e-5 * max(1.0, o.d_cf)
+    assert max(l.bank for l in ref.log) == 4
+    assert rel_l2(z.cpu().numpy(), ref.z) <= TOL_F32
