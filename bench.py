@@ -27,6 +27,11 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0
+# HBM traffic per launch of the dominant kernel from two rocprofv3 --pmc passes
+# (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, scale factors from a 1 GiB device
+# copy; profiles/attention_13b_hbm_traffic.md). Valid only for the kernel
+# version named here; set to None whenever that kernel changes.
+MEASURED_TRAFFIC = {"k_attn_bf16_pipe<128,1,2>": 53.726e9}
 METRIC = "DiT fwd TFLOP/s (% bf16 MFMA peak) + denoising steps/s at 13B shape"
 
 
@@ -196,7 +201,8 @@ def main():
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
-                     "traffic": None},
+                     "traffic": MEASURED_TRAFFIC.get("k_attn_bf16_pipe<128,1,2>") if args.workload == "13b" else None,
+                     "traffic_unit": "bytes per launch"},
     }
     if args.copy_probe > 0:
         src = torch.empty(args.copy_probe // 4, dtype=torch.float32, device=dev)
