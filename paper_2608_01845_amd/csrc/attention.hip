@@ -94,11 +94,21 @@ struct ACfg {
   static constexpr int LDS_BYTES = 2 * 2 * K_BYTES;  // 2 buffers x (K + V^T)
 };
 
-// K tile: rows of HD bf16 = HD/8 16-byte chunks; chunk c of row r at c ^ (r & 7)
+// LDS swizzles: 16 consecutive lanes read 16 different rows at one logical
+// chunk; the XOR spreads them over distinct bank groups of the 64 x 4-byte banks.
+// K tile: rows of HD bf16 = HD/8 16-byte chunks. hd = 128 (256-byte rows):
+// chunk c of row r at c ^ (r & 15); hd = 64 (128-byte rows, two per bank span):
+// c ^ ((r >> 1) & 7).
 template <int HD>
-__device__ __forceinline__ int kswz(int r, int c) { return (r * (HD / 8) + (c ^ (r & 7))) * 16; }
-// V^T tile: rows of 64 bf16 = 16 8-byte chunks; chunk c of row r at c ^ (r & 15)
-__device__ __forceinline__ int vswz(int r, int c) { return (r * 16 + (c ^ (r & 15))) * 8; }
+__device__ __forceinline__ int kswz(int r, int c) {
+  return HD == 128 ? (r * 16 + (c ^ (r & 15))) * 16 : (r * 8 + (c ^ ((r >> 1) & 7))) * 16;
+}
+// V^T tile: rows of 64 keys (128 B) = 8 16-byte slots. Within 16-key group j,
+// slot 2j holds keys 16j+[0,4) and 16j+8+[0,4), slot 2j+1 keys 16j+4+[0,4) and
+// 16j+12+[0,4): exactly the 8 keys lane group 0 / 1 feeds to one 32x32x16 step
+// of O^T = V^T P^T (the key order of the S^T accumulator), so each A operand is
+// one 16-byte read. Slot p of row r lives at p ^ ((r >> 1) & 7).
+__device__ __forceinline__ int vslot(int r, int p) { return (r * 8 + (p ^ ((r >> 1) & 7))) * 16; }
 
 template <int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
@@ -136,7 +146,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
   const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
   const int kst = kswz<HD>(kr, kc);            // same swizzle for every pass (KROWS % 8 == 0)
-  const int vst0 = vswz(vr, 2 * vc), vst1 = vswz(vr, 2 * vc + 1);
+  // global chunk vc = keys 8vc..8vc+7: first 4 keys -> slot 2(vc>>1), second 4 -> slot 2(vc>>1)+1,
+  // both in half (vc & 1) of the slot
+  const int vst0 = vslot(vr, 2 * (vc >> 1)) + (vc & 1) * 8, vst1 = vslot(vr, 2 * (vc >> 1) + 1) + (vc & 1) * 8;
 
   u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
 
@@ -159,12 +171,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   int kro[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4][2];
+  int vro[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    vro[j][0] = vswz(lr, 4 * j + lg);
-    vro[j][1] = vswz(lr, 4 * j + 2 + lg);
-  }
+  for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
 
   const int ntiles = (int)((a.n + KV - 1) / KV);
 #pragma unroll
@@ -274,10 +283,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < C::NH; ++i) {
         const char *vb = v + i * 32 * KV * 2;
-        const uint2 lo = *(const uint2 *)(vb + vro[j][0]);
-        const uint2 hi = *(const uint2 *)(vb + vro[j][1]);
-        u32x4 pk = {lo.x, lo.y, hi.x, hi.y};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, pk);
+        const bf16x8 vf = *(const bf16x8 *)(vb + vro[j]);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
           o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qt], o[i][qt], 0, 0, 0);
@@ -329,10 +335,19 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
   char *sK = smem;                     // [2][KV][HD]
   char *sV = smem + 2 * C::K_BYTES;    // [2][HD][KV]
 
-  const int h = blockIdx.y;
+  // Workgroups are dispatched round-robin over the 8 XCDs (linear id mod 8).
+  // With xcd_order, XCD x walks heads x, x+8, ... so the blocks resident on one
+  // XCD at a time belong to one head and share its K/V tiles in that XCD's L2.
+  int h = blockIdx.y, qb = blockIdx.x;
+  if (a.xcd_order) {
+    const int id = blockIdx.x + blockIdx.y * gridDim.x;
+    const int li = id >> 3;
+    h = (id & 7) + 8 * (li / gridDim.x);
+    qb = li % gridDim.x;
+  }
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qbase = (int64_t)blockIdx.x * C::QB + wid * C::QW;
+  const int64_t qbase = (int64_t)qb * C::QB + wid * C::QW;
   const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
 
   bf16x8 qf[QT][C::NS];
@@ -353,19 +368,19 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
   const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
   const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
   const int kst = kswz<HD>(kr, kc);
-  const int vst0 = vswz(vr, 2 * vc), vst1 = vswz(vr, 2 * vc + 1);
+  // global chunk vc = keys 8vc..8vc+7: first 4 keys -> slot 2(vc>>1), second 4 -> slot 2(vc>>1)+1,
+  // both in half (vc & 1) of the slot
+  const int vst0 = vslot(vr, 2 * (vc >> 1)) + (vc & 1) * 8, vst1 = vslot(vr, 2 * (vc >> 1) + 1) + (vc & 1) * 8;
   int kro[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4][2];
+  int vro[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    vro[j][0] = vswz(lr, 4 * j + lg);
-    vro[j][1] = vswz(lr, 4 * j + 2 + lg);
-  }
+  for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
 
   u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
   const int ntiles = (int)((a.n + KV - 1) / KV);
+  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
 
 #define WDC_LOAD_K(tile)                                                                          \
   _Pragma("unroll") for (int i = 0; i < C::K_CHUNKS; ++i) rk[i] =                                 \
@@ -435,15 +450,14 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
     f32x16 sn[2][QT];
     if (more_v) qk(sn, sK + ((t + 1) & 1) * C::K_BYTES);
 
-    const int64_t k0 = (int64_t)t * KV;
-    if (k0 + KV > a.n) {
+    if (!more_v && last_valid < KV) {
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= a.n) s[kt][qt][e] = -1e30f;
+            if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= last_valid) s[kt][qt][e] = -1e30f;
     }
     bool moved = false;
     float msc[QT];
@@ -491,10 +505,7 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < C::NH; ++i) {
         const char *vb = v + i * 32 * KV * 2;
-        const uint2 lo = *(const uint2 *)(vb + vro[j][0]);
-        const uint2 hi = *(const uint2 *)(vb + vro[j][1]);
-        u32x4 pk = {lo.x, lo.y, hi.x, hi.y};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, pk);
+        const bf16x8 vf = *(const bf16x8 *)(vb + vro[j]);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
           o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][qt], o[i][qt], 0, 0, 0);
@@ -566,14 +577,18 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
     // hd = 128: software-pipelined kernel, two blocks per CU; hd = 64: plain kernel
     // (both measured fastest at the workload shapes). WDC_ATTN_VARIANT overrides.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : -1;
+    static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
+    AttnArgs b = a;
+    b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
     if (a.hd == 128) {
-      if (variant == 0) return launch_bf16<128, 1>(a, s);
-      if (variant == 1) return launch_bf16_pipe<128, 1, 1>(a, s);
-      return launch_bf16_pipe<128, 1, 2>(a, s);
+      if (variant == 0) return launch_bf16<128, 1>(b, s);
+      if (variant == 1) return launch_bf16_pipe<128, 1, 1>(b, s);
+      if (variant == 3) return launch_bf16_pipe<128, 2, 1>(b, s);
+      return launch_bf16_pipe<128, 1, 2>(b, s);
     }
     if (a.hd == 64) {
-      if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(a, s);
-      return launch_bf16<64, 2>(a, s);
+      if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(b, s);
+      return launch_bf16<64, 2>(b, s);
     }
     return hipErrorInvalidValue;
   }

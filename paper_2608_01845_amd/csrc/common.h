@@ -108,6 +108,7 @@ struct AttnArgs {
   void *o;
   int64_t n, n_pad, ldo;
   int heads, hd;
+  int xcd_order;          // 1: blocks of one head run together on one XCD (heads % 8 == 0)
 };
 int64_t attn_pad(int64_t n);
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);

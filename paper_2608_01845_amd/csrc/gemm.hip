@@ -86,8 +86,10 @@ struct Cfg {
   static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
 };
 
-// Each tile row is 8 chunks of 16 bytes; chunk c of row r lives at c ^ (r & 7).
-__device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chunk ^ (row & 7))) * 16; }
+// Each tile row is 8 chunks of 16 bytes (128 B, two rows per 256-byte span of
+// the 64 LDS banks). Chunk c of row r lives at c ^ ((r >> 1) & 7), so the 16
+// rows read by 16 consecutive lanes land on 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chunk ^ ((row >> 1) & 7))) * 16; }
 
 template <int EPI>
 __device__ __forceinline__ float epi_act(float v) {

@@ -287,7 +287,7 @@ wdc_status gemv(wdc_ctx *c, const std::string &name, const float *x, float *y, i
 
 wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
   HIPCHK(c, launch_qkv_pad(c->d.dtype, c->q, c->k, c->v, c->H, c->hd, c->n, c->n_pad, c->stream));
-  AttnArgs a;
+  AttnArgs a{};
   a.q = c->q;
   a.k = c->k;
   a.v = c->v;
@@ -1213,7 +1213,7 @@ wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const v
                          int64_t ldo) {
   if (!ctx || !d_q || !d_k || !d_vt || !d_o || n <= 0) return WDC_E_ARG;
   if (!aligned16(d_q) || !aligned16(d_k) || !aligned16(d_vt)) return WDC_E_ALIGN;
-  AttnArgs a;
+  AttnArgs a{};
   a.q = d_q;
   a.k = d_k;
   a.v = d_vt;
