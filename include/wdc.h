@@ -216,10 +216,12 @@ wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const
 /* ---------------------------------------------------------------- kernels exposed for tests and benchmarks */
 
 /* softmax(q k^T / sqrt(hd)) v over the full sequence, the attention of every
- * block. d_q, d_k: [heads, n_pad, hd]; d_vt: [heads, hd, n_pad] (keys
- * contiguous) for bf16, [heads, n_pad, hd] for float32; n valid tokens,
- * n_pad = wdc_attn_pad(n); rows >= n of q/k/v must be zero. d_o: [n, ldo],
- * head h written at columns [h*hd, (h+1)*hd). */
+ * block. d_q, d_k: [heads, n_pad, hd]. d_vt for bf16: [heads, hd, n_pad], V
+ * transposed with the keys of each aligned group of 16 stored in the order
+ * 0-3, 8-11, 4-7, 12-15 (key j at column j with bits 2 and 3 swapped); for
+ * float32: [heads, n_pad, hd]. n valid tokens, n_pad = wdc_attn_pad(n); rows
+ * (keys) >= n of q/k/v must be zero. d_o: [n, ldo], head h written at columns
+ * [h*hd, (h+1)*hd). */
 int64_t wdc_attn_pad(int64_t n);
 wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
                          int64_t ldo);

@@ -81,6 +81,7 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a) {
 // ---------------------------------------------------------------- bf16 flash attention on MFMA
 constexpr int KV = 64;                   // keys per LDS tile
 constexpr int RSRC_WORD3 = 0x00020000;   // raw buffer descriptor word 3
+constexpr int WAIT_VM0 = 0x0F70;         // s_waitcnt vmcnt(0), other counters untouched
 
 template <int HD, int QT>
 struct ACfg {
@@ -110,6 +111,37 @@ __device__ __forceinline__ int kswz(int r, int c) {
 // one 16-byte read. Slot p of row r lives at p ^ ((r >> 1) & 7).
 __device__ __forceinline__ int vslot(int r, int p) { return (r * 8 + (p ^ ((r >> 1) & 7))) * 16; }
 
+// Direct global -> LDS tile loads (buffer_load_dwordx4 ... lds): lane L of a
+// wavefront's load writes its 16 bytes at LDS base + 16 L, so the swizzles above
+// are applied by choosing which global chunk each lane fetches. Wave w of 4
+// fills 1 KB stripes w, w+4, w+8, ... of each tile:
+//   K tile:   stripe holds rows [r0, r0 + 1024/(2 HD)) of 2 HD bytes;
+//   V^T tile: stripe holds 8 rows of 128 bytes (the global V^T rows are stored
+//             with the slot key order already applied, see k_v_transpose).
+// Stripe i of wave w starts at LDS byte w*1024 + i*4096 in both tiles; the row
+// swizzle keys are the same for every stripe of a wave, so one VGPR offset per
+// tile kind plus a uniform SGPR offset per stripe addresses the global side.
+typedef __attribute__((address_space(3))) void lds_void;
+// (kept out of line of the kernel templates: called directly from a template
+// kernel body the builtin makes the host pass drop the kernel's launch stub)
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, char *lds, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, voff, soff, 0, 0);
+}
+template <int HD>
+struct TileLoad {
+  static constexpr int K_ROWS = 1024 / (2 * HD);   // K rows per 1 KB stripe (4 or 8)
+  static constexpr int K_STRIPES = 16 / K_ROWS;    // stripes per wave per K tile (4 or 2)
+  static constexpr int V_STRIPES = HD / 32;        // stripes per wave per V^T tile (4 or 2)
+  int kvo, vvo;                                    // per-lane global byte offsets (stripe 0, tile 0)
+  __device__ __forceinline__ TileLoad(int w, int lane, int64_t n_pad) {
+    const int kr0 = w * K_ROWS + lane / (HD / 8), kps = lane % (HD / 8);
+    const int kc = HD == 128 ? (kps ^ (kr0 & 15)) : (kps ^ ((kr0 >> 1) & 7));
+    kvo = kr0 * HD * 2 + kc * 16;
+    const int vr0 = 8 * w + lane / 8, vps = lane % 8;
+    vvo = vr0 * (int)n_pad * 2 + (vps ^ ((vr0 >> 1) & 7)) * 16;
+  }
+};
+
 template <int HD, int QT>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   using C = ACfg<HD, QT>;
@@ -137,20 +169,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
   const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
       (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  // chunk i of this thread: K row tid/(HD/8) + i*(256/(HD/8)), chunk tid%(HD/8);
-  //                         V^T row tid/8 + 32 i, chunk tid%8
-  constexpr int KCPR = HD / 8, KROWS = 256 / KCPR;
-  const int kr = tid / KCPR, kc = tid % KCPR;
-  const int vr = tid >> 3, vc = tid & 7;
-  const int kvoff = kr * HD * 2 + kc * 16;
-  const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
-  const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
-  const int kst = kswz<HD>(kr, kc);            // same swizzle for every pass (KROWS % 8 == 0)
-  // global chunk vc = keys 8vc..8vc+7: first 4 keys -> slot 2(vc>>1), second 4 -> slot 2(vc>>1)+1,
-  // both in half (vc & 1) of the slot
-  const int vst0 = vslot(vr, 2 * (vc >> 1)) + (vc & 1) * 8, vst1 = vslot(vr, 2 * (vc >> 1) + 1) + (vc & 1) * 8;
-
-  u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
+  const int wu = __builtin_amdgcn_readfirstlane(wid);
+  const TileLoad<HD> tl(wu, lane, a.n_pad);
+  using TL = TileLoad<HD>;
+#define WDC_TILE_LOAD(KOFF, VOFF, tile)                                                             \
+  {                                                                                                 \
+    _Pragma("unroll") for (int i = 0; i < TL::K_STRIPES; ++i)                                       \
+        lds_load16(kdesc, sK + (KOFF) + wu * 1024 + i * 4096, tl.kvo, (tile) * KV * HD * 2 + i * 4096); \
+    _Pragma("unroll") for (int i = 0; i < TL::V_STRIPES; ++i)                                       \
+        lds_load16(vdesc, sV + (VOFF) + wu * 1024 + i * 4096, tl.vvo,                                \
+                   (tile) * KV * 2 + i * 32 * (int)a.n_pad * 2);                                     \
+  }
 
   f32x16 o[C::NH][QT];
 #pragma unroll
@@ -176,31 +205,14 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
 
   const int ntiles = (int)((a.n + KV - 1) / KV);
-#pragma unroll
-  for (int i = 0; i < C::K_CHUNKS; ++i) rk[i] = __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass, 0);
-#pragma unroll
-  for (int i = 0; i < C::V_CHUNKS; ++i) rv[i] = __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass, 0);
-#pragma unroll
-  for (int i = 0; i < C::K_CHUNKS; ++i) *(u32x4 *)(sK + kst + i * KROWS * HD * 2) = rk[i];
-#pragma unroll
-  for (int i = 0; i < C::V_CHUNKS; ++i) {
-    *(uint2 *)(sV + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);
-    *(uint2 *)(sV + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);
-  }
+  WDC_TILE_LOAD(0, 0, 0);
+  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
     const bool more = t + 1 < ntiles;
-    if (more) {
-      const int kb = (t + 1) * KV * HD * 2, vb = (t + 1) * KV * 2;
-#pragma unroll
-      for (int i = 0; i < C::K_CHUNKS; ++i)
-        rk[i] = __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass + kb, 0);
-#pragma unroll
-      for (int i = 0; i < C::V_CHUNKS; ++i)
-        rv[i] = __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass + vb, 0);
-    }
+    if (more) WDC_TILE_LOAD((buf ^ 1) * C::K_BYTES, (buf ^ 1) * C::K_BYTES, t + 1);
     const char *k = sK + buf * C::K_BYTES, *v = sV + buf * C::K_BYTES;
 
     // S^T = K Q^T: [2 key tiles][QT query tiles]
@@ -289,18 +301,10 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
           o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qt], o[i][qt], 0, 0, 0);
       }
     }
-    if (more) {
-      char *nk = sK + (buf ^ 1) * C::K_BYTES, *nv = sV + (buf ^ 1) * C::K_BYTES;
-#pragma unroll
-      for (int i = 0; i < C::K_CHUNKS; ++i) *(u32x4 *)(nk + kst + i * KROWS * HD * 2) = rk[i];
-#pragma unroll
-      for (int i = 0; i < C::V_CHUNKS; ++i) {
-        *(uint2 *)(nv + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);
-        *(uint2 *)(nv + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);
-      }
-    }
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     __syncthreads();
   }
+#undef WDC_TILE_LOAD
   // normalise and store: lane holds query 32qt + lr, hd 32i + 8(e/4) + 4lg + e%4
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
@@ -361,16 +365,9 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
       (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
   const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
       (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  constexpr int KCPR = HD / 8, KROWS = 256 / KCPR;
-  const int kr = tid / KCPR, kc = tid % KCPR;
-  const int vr = tid >> 3, vc = tid & 7;
-  const int kvoff = kr * HD * 2 + kc * 16;
-  const int vvoff = vr * (int)a.n_pad * 2 + vc * 16;
-  const int kpass = KROWS * HD * 2, vpass = 32 * (int)a.n_pad * 2;
-  const int kst = kswz<HD>(kr, kc);
-  // global chunk vc = keys 8vc..8vc+7: first 4 keys -> slot 2(vc>>1), second 4 -> slot 2(vc>>1)+1,
-  // both in half (vc & 1) of the slot
-  const int vst0 = vslot(vr, 2 * (vc >> 1)) + (vc & 1) * 8, vst1 = vslot(vr, 2 * (vc >> 1) + 1) + (vc & 1) * 8;
+  const int wu = __builtin_amdgcn_readfirstlane(wid);
+  const TileLoad<HD> tl(wu, lane, a.n_pad);
+  using TL = TileLoad<HD>;
   int kro[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
@@ -378,34 +375,22 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
 
-  u32x4 rk[C::K_CHUNKS], rv[C::V_CHUNKS];
   const int ntiles = (int)((a.n + KV - 1) / KV);
   const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
 
-#define WDC_LOAD_K(tile)                                                                          \
-  _Pragma("unroll") for (int i = 0; i < C::K_CHUNKS; ++i) rk[i] =                                 \
-      __builtin_amdgcn_raw_buffer_load_b128(kdesc, kvoff, i * kpass + (tile) * KV * HD * 2, 0)
-#define WDC_LOAD_V(tile)                                                                          \
-  _Pragma("unroll") for (int i = 0; i < C::V_CHUNKS; ++i) rv[i] =                                 \
-      __builtin_amdgcn_raw_buffer_load_b128(vdesc, vvoff, i * vpass + (tile) * KV * 2, 0)
-#define WDC_STORE_K(b)                                                                            \
-  _Pragma("unroll") for (int i = 0; i < C::K_CHUNKS; ++i)                                         \
-      *(u32x4 *)(sK + (b) * C::K_BYTES + kst + i * KROWS * HD * 2) = rk[i]
-#define WDC_STORE_V(b)                                                                            \
-  _Pragma("unroll") for (int i = 0; i < C::V_CHUNKS; ++i) {                                       \
-    *(uint2 *)(sV + (b) * C::K_BYTES + vst0 + i * 32 * KV * 2) = make_uint2(rv[i].x, rv[i].y);     \
-    *(uint2 *)(sV + (b) * C::K_BYTES + vst1 + i * 32 * KV * 2) = make_uint2(rv[i].z, rv[i].w);     \
-  }
+#define WDC_LOAD_K(b, tile)                                                                          \
+  _Pragma("unroll") for (int i = 0; i < TL::K_STRIPES; ++i)                                          \
+      lds_load16(kdesc, sK + (b) * C::K_BYTES + wu * 1024 + i * 4096, tl.kvo, (tile) * KV * HD * 2 + i * 4096)
+#define WDC_LOAD_V(b, tile)                                                                          \
+  _Pragma("unroll") for (int i = 0; i < TL::V_STRIPES; ++i)                                          \
+      lds_load16(vdesc, sV + (b) * C::K_BYTES + wu * 1024 + i * 4096, tl.vvo,                              \
+                 (tile) * KV * 2 + i * 32 * (int)a.n_pad * 2)
 
   // prologue: K_0, V_0, K_1
-  WDC_LOAD_K(0);
-  WDC_LOAD_V(0);
-  WDC_STORE_K(0);
-  WDC_STORE_V(0);
-  if (ntiles > 1) {
-    WDC_LOAD_K(1);
-    WDC_STORE_K(1);
-  }
+  WDC_LOAD_K(0, 0);
+  WDC_LOAD_V(0, 0);
+  if (ntiles > 1) WDC_LOAD_K(1, 1);
+  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   __syncthreads();
 
   f32x16 o[C::NH][QT];
@@ -444,9 +429,10 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
   qk(s, sK);
 
   for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
     const bool more_k = t + 2 < ntiles, more_v = t + 1 < ntiles;
-    if (more_k) WDC_LOAD_K(t + 2);
-    if (more_v) WDC_LOAD_V(t + 1);
+    if (more_k) WDC_LOAD_K(buf, t + 2);          // kbuf[t&1] held K_t, read last iteration
+    if (more_v) WDC_LOAD_V(buf ^ 1, t + 1);      // vbuf[(t+1)&1] held V_{t-1}, read last iteration
     f32x16 sn[2][QT];
     if (more_v) qk(sn, sK + ((t + 1) & 1) * C::K_BYTES);
 
@@ -511,8 +497,7 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
           o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][qt], o[i][qt], 0, 0, 0);
       }
     }
-    if (more_k) WDC_STORE_K(t & 1);
-    if (more_v) WDC_STORE_V((t + 1) & 1);
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     __syncthreads();
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -521,8 +506,6 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
   }
 #undef WDC_LOAD_K
 #undef WDC_LOAD_V
-#undef WDC_STORE_K
-#undef WDC_STORE_V
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);

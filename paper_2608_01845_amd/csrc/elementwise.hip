@@ -109,6 +109,11 @@ __global__ __launch_bounds__(256) void k_v_copy(QKVPrepArgs a) {
   ((T *)a.v)[((int64_t)h * a.n_pad + a.row0 + r) * a.hd + e] = *src;
 }
 
+// Position of key j in a V^T row: inside each aligned group of 16 keys the
+// order is 0-3, 8-11, 4-7, 12-15 (bits 2 and 3 of j swapped), which makes the 8
+// keys one lane feeds to an O^T = V^T P^T step one 16-byte chunk.
+__device__ __forceinline__ int64_t vt_pos(int64_t j) { return (j & ~(int64_t)12) | ((j & 4) << 1) | ((j & 8) >> 1); }
+
 // v rows -> transposed [H, hd, n_pad] through a 64-row LDS tile, so that both
 // the reads (rows of the projection output) and the writes (runs of 64 tokens)
 // are coalesced.
@@ -127,7 +132,7 @@ __global__ __launch_bounds__(256) void k_v_transpose(QKVPrepArgs a) {
   for (int idx = threadIdx.x; idx < 64 * a.hd; idx += 256) {
     int e = idx / 64, rr = idx % 64;
     int64_t r = r0 + rr;
-    if (r < a.rows) ((bf16_t *)a.v)[((int64_t)h * a.hd + e) * a.n_pad + a.row0 + r] = tile[rr][e];
+    if (r < a.rows) ((bf16_t *)a.v)[((int64_t)h * a.hd + e) * a.n_pad + vt_pos(a.row0 + r)] = tile[rr][e];
   }
 }
 
@@ -144,7 +149,7 @@ __global__ void k_qkv_pad(T *q, T *k, T *v, int heads, int hd, int64_t n, int64_
     q[o] = 0;
     k[o] = 0;
     if (v_transposed)
-      v[((int64_t)h * hd + e) * n_pad + row] = 0;
+      v[((int64_t)h * hd + e) * n_pad + vt_pos(row)] = 0;
     else
       v[o] = 0;
   }

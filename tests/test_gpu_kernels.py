@@ -59,7 +59,15 @@ def _attn_inputs(ctx, heads, hd, n, seed, bf16):
         return out
     qd, kd = ctx.to_device(pad(q)), ctx.to_device(pad(k))
     vp = pad(v)
-    vd = ctx.to_device(np.ascontiguousarray(vp.transpose(0, 2, 1)) if bf16 else vp)
+    if bf16:
+        # V^T layout of the bf16 kernel: key j stored at column j with bits 2 and 3 swapped
+        j = np.arange(npad)
+        pos = (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1)
+        vt = np.zeros((heads, hd, npad), np.float32)
+        vt[:, :, pos] = vp.transpose(0, 2, 1)
+        vd = ctx.to_device(vt)
+    else:
+        vd = ctx.to_device(vp)
     return (q, k, v), (qd, kd, vd)
 
 
