@@ -5,8 +5,8 @@
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 tiles, BMxBN block tile, BK = 64,
 // double-buffered LDS with an XOR swizzle of the 16-byte chunks of each
-// 128-byte row (conflict-free fragment reads), the next K tile prefetched into
-// registers while the current one feeds the matrix cores.
+// 128-byte row (conflict-free fragment reads), the next K tile loaded straight
+// from HBM into the other LDS buffer while the current one feeds the matrix cores.
 // float32 path (tiny fp32 workload, and shapes the MFMA tiles do not cover):
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
@@ -74,15 +74,22 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g) {
 // ---------------------------------------------------------------- bf16 MFMA kernel
 constexpr int BK = 64;  // K per LDS stage: one 128-byte row of bf16 per tile row
 constexpr int RSRC_WORD3 = 0x00020000;  // raw buffer: 32-bit data format, no swizzle
+constexpr int WAIT_VM0 = 0x0F70;        // s_waitcnt vmcnt(0), other counters untouched
+
+typedef __attribute__((address_space(3))) void lds_void;
+// 16 bytes per lane from a buffer straight into LDS (lane L at lds + 16 L); kept
+// out of the kernel templates, where the builtin makes the host pass drop stubs
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, char *lds, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, voff, soff, 0, 0);
+}
 
 template <int BM, int BN, int WM, int WN>
 struct Cfg {
   static constexpr int NT = 64 * WM * WN;       // threads
   static constexpr int TM = BM / WM / 32;       // 32x32 tiles per wave along M
   static constexpr int TN = BN / WN / 32;       // along N
-  static constexpr int A_CHUNKS = BM * 8 / NT;  // 16-byte chunks per thread per stage
+  static constexpr int A_CHUNKS = BM * 8 / NT;  // 1 KB stripes per wave per stage (= chunks per thread)
   static constexpr int B_CHUNKS = BN * 8 / NT;
-  static constexpr int ROWS_PER_PASS = NT / 8;  // tile rows covered by one chunk index
   static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
 };
 
@@ -126,18 +133,29 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
   const int wm = wid / WN, wn = wid % WN;
   const int lr = lane & 31, lg = lane >> 5;
 
-  // buffer descriptors over this block's A rows and W rows; rows past m read as 0
+  // Tiles go straight from HBM to LDS (buffer_load_dwordx4 ... lds: lane L of a
+  // wavefront's load writes 16 bytes at LDS base + 16 L). Stripe s = 1 KB = 8
+  // tile rows; wave w loads stripes w, w + NW, w + 2 NW, ... so each lane fetches
+  // row 8s + lane/8 and the logical chunk that the swizzle puts at physical
+  // chunk lane%8 (the swizzle key (row >> 1) & 7 is the same for every stripe
+  // of a wave since NW is even).
+  // The A descriptor spans only this block's valid rows and every stripe's row
+  // is in the VGPR offset, which the buffer range check covers: rows past m are
+  // read as zero (the K offset rides in the SGPR offset and is always in range).
+  constexpr int NW = C::NT / 64;
+  static_assert(NW % 2 == 0, "stripe swizzle assumes an even wave count");
   const int64_t rows_a = min((int64_t)BM, g.m - m0);
-  const __amdgpu_buffer_rsrc_t ra_desc = __builtin_amdgcn_make_buffer_rsrc(
+  const __amdgpu_buffer_rsrc_t a_desc = __builtin_amdgcn_make_buffer_rsrc(
       (void *)((const bf16_t *)g.a + m0 * g.lda), (short)0, (int)(rows_a * g.lda * 2), RSRC_WORD3);
-  const __amdgpu_buffer_rsrc_t rb_desc = __builtin_amdgcn_make_buffer_rsrc(
+  const __amdgpu_buffer_rsrc_t b_desc = __builtin_amdgcn_make_buffer_rsrc(
       (void *)((const bf16_t *)g.w + n0 * g.k), (short)0, (int)(BN * g.k * 2), RSRC_WORD3);
-  const int crow = tid >> 3, cch = tid & 7;
-  const int va = crow * (int)g.lda * 2 + cch * 16;     // byte offset of this thread's chunk (pass 0)
-  const int vb = crow * (int)g.k * 2 + cch * 16;
-  const int pass_a = C::ROWS_PER_PASS * (int)g.lda * 2;
-  const int pass_b = C::ROWS_PER_PASS * (int)g.k * 2;
-  const int st_off = swz(crow, cch);                    // LDS byte offset of pass 0 (same swizzle every pass)
+  const int wu = __builtin_amdgcn_readfirstlane(wid);
+  const int lch = (lane & 7) ^ ((4 * (wu & 1) + (lane >> 4)) & 7);
+  const int row0 = 8 * wu + (lane >> 3);
+  int va[C::A_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < C::A_CHUNKS; ++i) va[i] = (row0 + 8 * NW * i) * (int)g.lda * 2 + lch * 16;
+  const int vb = row0 * (int)g.k * 2 + lch * 16;
 
   // fragment read offsets: row wm*(BM/WM) + 32i + lr, chunk 2s + lg (swizzle depends on lr only)
   int ra_off[4], rb_off[4];
@@ -147,9 +165,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
     rb_off[s] = swz(wn * (BN / WN) + lr, 2 * s + lg);
   }
 
-  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-  u32x4 ra[C::A_CHUNKS], rb[C::B_CHUNKS];
-
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
   for (int i = 0; i < C::TM; ++i)
@@ -158,30 +173,23 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+#define WDC_GEMM_LOAD(buf, kt)                                                                     \
+  {                                                                                                \
+    const int kb_ = (kt) * BK * 2;                                                                 \
+    _Pragma("unroll") for (int i = 0; i < C::A_CHUNKS; ++i)                                         \
+        lds_load16(a_desc, sA + (buf) * BM * 128 + (i * NW + wu) * 1024, va[i], kb_);               \
+    _Pragma("unroll") for (int i = 0; i < C::B_CHUNKS; ++i)                                         \
+        lds_load16(b_desc, sB + (buf) * BN * 128 + (i * NW + wu) * 1024, vb, i * 8 * NW * (int)g.k * 2 + kb_); \
+  }
+
   const int nk = (int)(g.k / BK);
-  // prologue: tile 0
-#pragma unroll
-  for (int i = 0; i < C::A_CHUNKS; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(ra_desc, va, i * pass_a, 0);
-#pragma unroll
-  for (int i = 0; i < C::B_CHUNKS; ++i) rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb_desc, vb, i * pass_b, 0);
-#pragma unroll
-  for (int i = 0; i < C::A_CHUNKS; ++i) *(u32x4 *)(sA + st_off + i * C::ROWS_PER_PASS * 128) = ra[i];
-#pragma unroll
-  for (int i = 0; i < C::B_CHUNKS; ++i) *(u32x4 *)(sB + st_off + i * C::ROWS_PER_PASS * 128) = rb[i];
+  WDC_GEMM_LOAD(0, 0);
+  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   __syncthreads();
 
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int kb = (kt + 1) * BK * 2;
-#pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i)
-        ra[i] = __builtin_amdgcn_raw_buffer_load_b128(ra_desc, va, i * pass_a + kb, 0);
-#pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i)
-        rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rb_desc, vb, i * pass_b + kb, 0);
-    }
+    if (kt + 1 < nk) WDC_GEMM_LOAD(buf ^ 1, kt + 1);   // buffer buf^1 was last read in iteration kt-1
     const char *a = sA + buf * BM * 128, *b = sB + buf * BN * 128;
 #pragma unroll
     for (int s = 0; s < BK / 16; ++s) {
@@ -196,15 +204,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
         for (int j = 0; j < C::TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
-    if (more) {
-      char *na = sA + (buf ^ 1) * BM * 128, *nb = sB + (buf ^ 1) * BN * 128;
-#pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i) *(u32x4 *)(na + st_off + i * C::ROWS_PER_PASS * 128) = ra[i];
-#pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i) *(u32x4 *)(nb + st_off + i * C::ROWS_PER_PASS * 128) = rb[i];
-    }
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     __syncthreads();
   }
+#undef WDC_GEMM_LOAD
 
   // epilogue: lane holds column lr of each 32x32 tile, rows 8*(e/4) + 4*lg + e%4
   const bf16_t *bias = (const bf16_t *)g.bias;
