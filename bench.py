@@ -197,11 +197,11 @@ def main():
                     "attention_tflops": round(att_tflops, 1) if att_tflops else None,
                     "gemm_ms_total": round(gemm_ms, 1), "gemm_launches": gemm_n,
                     "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None},
-        "roofline": {"bound": "mfma", "kernel": "k_attn_bf16_pipe<128,1,2>",
+        "roofline": {"bound": "mfma", "kernel": "k_attn_bf16_pp<128>",
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
-                     "traffic": MEASURED_TRAFFIC.get("k_attn_bf16_pipe<128,1,2>") if args.workload == "13b" else None,
+                     "traffic": MEASURED_TRAFFIC.get("k_attn_bf16_pp<128>") if args.workload == "13b" else None,
                      "traffic_unit": "bytes per launch"},
     }
     if args.copy_probe > 0:
