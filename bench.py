@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--workload", default="13b", choices=["13b", "5b", "mid", "tiny"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
     ap.add_argument("--surrogate-steps", type=int, default=20)
+    ap.add_argument("--no-surrogate", action="store_true", help="skip the standalone surrogate-kernel leg")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="also run one plain device copy of this many bytes (hardware-counter calibration)")
     return ap.parse_args()
@@ -80,6 +81,66 @@ def cpu_baseline(cfg, rows: int = 64):
             "kind": "oracle", "seconds": dt,
             "sample": f"one {kind} block of the {cfg.name} workload in float64: keys/values for all {n} tokens, "
                       f"queries/attention/MLP for {rows} sampled rows ({flops / 1e12:.2f} TFLOP)"}
+
+
+def hbm_entry(ms, launches, nbytes):
+    """Average launch time and achieved algorithmic bandwidth of one HBM-bound kernel class."""
+    if not launches:
+        return None
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"launches": launches, "ms_avg": round(ms / launches, 4), "bytes_per_launch": round(nbytes / launches),
+            "GB/s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 3)}
+
+
+def surrogate_leg(wdc, synth, torch, dev, steps=24):
+    """The surrogate and risk kernels alone on the largest latent (16x33x90x160
+    float32) with a bank of 4 records: one replay rollout (exact every 4th step,
+    recorded velocities standing in for F_theta), then the pass-1 statistics
+    kernel on its own through the step-by-step entry point."""
+    cfg = synth.get_config("stress")
+    ctx = wdc.Context(cfg, device=str(dev), allocate_weights=False)
+    st = ctx.new_state()
+    gen = torch.Generator(device=dev).manual_seed(cfg.seed)
+    lat = tuple(cfg.latent)
+    z0 = torch.randn(lat, generator=gen, device=dev)
+    base = torch.randn(lat, generator=gen, device=dev)
+    vel = torch.empty((steps,) + lat, device=dev)
+    for k in range(steps):
+        vel[k] = base + 0.3 * torch.randn(lat, generator=gen, device=dev)
+    mask = [0 if k % 4 == 0 else 1 for k in range(steps)]
+    z = z0.clone()
+    ctx.rollout(st, z, steps, mode=wdc.MODE_FORCED, forced=mask, replay_v=vel)    # warm-up
+    z.copy_(z0)
+    torch.cuda.synchronize()
+    ctx.set_timing(True)
+    t0 = time.perf_counter()
+    sched, logs = ctx.rollout(st, z, steps, mode=wdc.MODE_FORCED, forced=mask, replay_v=vel)
+    wall = time.perf_counter() - t0
+    tm = ctx.timing()
+    ctx.set_timing(False)
+    # pass 1 alone (the rollout emits it from the observation / epilogue kernels)
+    zhat = torch.empty_like(z)
+    ctx.set_timing(True)
+    step_ms = []
+    for i in range(20):
+        t1 = time.perf_counter()
+        ctx.surrogate_step(st, z, steps - 1, steps, zhat)
+        ctx.risk_update(st, wdc.PRE_DECISION, steps - 1, steps)
+        step_ms.append((time.perf_counter() - t1) * 1e3)
+    tp = ctx.timing()
+    ctx.set_timing(False)
+    n_sur = sum(sched)
+    res = {"workload": f"latent {'x'.join(map(str, cfg.latent))} float32 ({cfg.numel} elements), bank of 4; "
+                       f"replay rollout of {steps} steps, exact every 4th ({steps - n_sur} exact, {n_sur} surrogate)",
+           "observe": hbm_entry(*tm["observe"]), "exact_post": hbm_entry(*tm["exact_post"]),
+           "stats": hbm_entry(*tp["stats"]),
+           "rollout_ms_per_step": round(wall / steps * 1e3, 3),
+           "surrogate_step_ms_median": round(float(sorted(step_ms)[len(step_ms) // 2]), 3),
+           "note": "bytes = each input read once + each output written once; rollout time includes one "
+                   "host synchronisation per step for the float64 controller"}
+    del ctx, st, z, z0, base, vel, zhat
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -155,14 +216,14 @@ def main():
         sur_ms.append((time.perf_counter() - t1) * 1e3)
     sur_med = float(np.median(sur_ms))
 
-    # roofline of the dominant kernel (attention: 4 N^2 D per block)
-    att_ms, att_n = timing["attention"]
+    # roofline of the dominant kernel (attention: 4 N^2 D per block), from the
+    # library's HIP events on its own stream over the timed steps
+    att_ms, att_n, att_work = timing["attention"]
     att_avg_ms = att_ms / max(att_n, 1)
-    att_flops = 4.0 * cfg.n_tokens ** 2 * cfg.hidden
-    att_tflops = att_flops / (att_avg_ms / 1e3) / 1e12 if att_n else None
-    gemm_ms, gemm_n = timing["gemm"]
-    lin_flops = 24.0 * cfg.n_tokens * cfg.hidden ** 2 * cfg.n_blocks * args.steps
-    gemm_tflops = lin_flops / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
+    att_tflops = att_work / (att_ms / 1e3) / 1e12 if att_n else None
+    gemm_ms, gemm_n, gemm_work = timing["gemm"]
+    gemm_tflops = gemm_work / (gemm_ms / 1e3) / 1e12 if gemm_ms else None
+    norm_ms, norm_n, norm_work = timing["norm"]
 
     exact_ratio = 0.20
     n_exact = round(exact_ratio * S)
@@ -196,7 +257,8 @@ def main():
         "kernels": {"attention_ms_avg": round(att_avg_ms, 3), "attention_launches": att_n,
                     "attention_tflops": round(att_tflops, 1) if att_tflops else None,
                     "gemm_ms_total": round(gemm_ms, 1), "gemm_launches": gemm_n,
-                    "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None},
+                    "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None,
+                    "layernorm_modulate": hbm_entry(norm_ms, norm_n, norm_work)},
         "roofline": {"bound": "mfma", "kernel": "k_attn_bf16_pp<128>",
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -204,6 +266,10 @@ def main():
                      "traffic": MEASURED_TRAFFIC.get("k_attn_bf16_pp<128>") if args.workload == "13b" else None,
                      "traffic_unit": "bytes per launch"},
     }
+    del ctx, st, z, zbuf, zhat, v, cond, text, cam
+    torch.cuda.empty_cache()
+    if not args.no_surrogate:
+        out["surrogate_kernels"] = surrogate_leg(wdc, synth, torch, dev)
     if args.copy_probe > 0:
         src = torch.empty(args.copy_probe // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)

@@ -231,11 +231,27 @@ wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const v
 wdc_status wdc_linear(wdc_ctx *ctx, const void *d_a, int64_t lda, const void *d_w, const void *d_bias, void *d_c,
                       int64_t ldc, int64_t m, int64_t n, int64_t k);
 
-/* Seconds of GPU time of the last kernel of each class launched by this context
- * when timing is on (wdc_set_timing(ctx, 1)); used by benchmarks. Index 0:
- * attention, 1: GEMM, 2: everything else. */
+/* Kernel timing for benchmarks. While timing is on (wdc_set_timing(ctx, 1),
+ * which also clears the totals), every launch of the classes below on the
+ * context's stream is bracketed by HIP events; wdc_timing synchronises the
+ * stream and returns, per class, the summed milliseconds, the number of
+ * launches and (out_work, may be NULL) the summed algorithmic work of those
+ * launches: FLOPs for the matrix classes (attention 4 n^2 hd per head, GEMM
+ * 2 m n k), bytes that must cross HBM for the streaming classes (each input
+ * read once, each output written once). Off by default (no events). */
+enum {
+  WDC_T_ATTENTION = 0,  /* flash attention */
+  WDC_T_GEMM = 1,       /* linear layers */
+  WDC_T_STATS = 2,      /* pass-1 lift statistics of a latent (Eq. (2), (6)) */
+  WDC_T_OBSERVE = 3,    /* kernel observation combine (Eq. (5)) */
+  WDC_T_EXACT_POST = 4, /* exact-step epilogue: Psi, counterfactual sums, bank and anchor writes */
+  WDC_T_PSI = 5,        /* standalone scheduler step (wdc_scheduler_step) */
+  WDC_T_NORM = 6,       /* LayerNorm + modulation of the residual stream */
+  WDC_T_COUNT = 7
+};
 wdc_status wdc_set_timing(wdc_ctx *ctx, int32_t on);
-wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[3], int64_t out_count[3]);
+wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[WDC_T_COUNT], int64_t out_count[WDC_T_COUNT],
+                      double out_work[WDC_T_COUNT]);
 
 #ifdef __cplusplus
 }

@@ -20,6 +20,8 @@ WDC_F32, WDC_BF16 = 0, 1
 MODE_RISK, MODE_FORCED, MODE_ALL_EXACT = 0, 1, 2
 PRE_DECISION, POST_EXACT, POST_SURROGATE = 0, 1, 2
 MAX_BANK = 8
+# kernel timing classes, in the order of the WDC_T_* constants
+TIMING_CLASSES = ("attention", "gemm", "stats", "observe", "exact_post", "psi", "norm")
 STATUS = {0: "OK", 1: "E_ARG", 2: "E_SHAPE", 3: "E_DTYPE", 4: "E_ALIGN", 5: "E_WORKSPACE", 6: "E_STATE",
           7: "E_HIP", 8: "E_NONFINITE", 9: "E_UNSUPPORTED"}
 
@@ -110,7 +112,7 @@ def load() -> C.CDLL:
         "wdc_attention": (i32, [vp, vp, vp, vp, i64, vp, i64]),
         "wdc_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, i64, i64]),
         "wdc_set_timing": (i32, [vp, i32]),
-        "wdc_timing": (i32, [vp, C.POINTER(dbl), C.POINTER(i64)]),
+        "wdc_timing": (i32, [vp, C.POINTER(dbl), C.POINTER(i64), C.POINTER(dbl)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -284,10 +286,10 @@ class Context:
         self._check(self.lib.wdc_set_timing(self.h, int(on)))
 
     def timing(self):
-        ms = (C.c_double * 3)()
-        cnt = (C.c_int64 * 3)()
-        self._check(self.lib.wdc_timing(self.h, ms, cnt))
-        return {"attention": (ms[0], cnt[0]), "gemm": (ms[1], cnt[1]), "other": (ms[2], cnt[2])}
+        n = len(TIMING_CLASSES)
+        ms, cnt, work = (C.c_double * n)(), (C.c_int64 * n)(), (C.c_double * n)()
+        self._check(self.lib.wdc_timing(self.h, ms, cnt, work))
+        return {name: (ms[i], cnt[i], work[i]) for i, name in enumerate(TIMING_CLASSES)}
 
     # ---------------------------------------------------------------- surrogate, risk, rollout
     def new_state(self) -> "State":

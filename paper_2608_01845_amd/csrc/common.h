@@ -162,22 +162,26 @@ struct SegPlan {
   int64_t t;
   int g;       // chunks per channel (8)
   int splits;  // blocks per segment
+  int vec;     // 16-byte vector access (set per launch from the buffers' alignment)
   int nseg() const { return c * g; }
   int nblocks() const { return c * g * splits; }
 };
 SegPlan make_seg_plan(int c, int64_t t, int g);
 
-// values per block of each stats kernel
-enum { PRE_NV = 6, POST_NV = 9, OBS_NV = 1 };
+// values per block of each stats kernel; the observation kernel emits the
+// PRE_NV statistics of zhat (against its anchor) and then a non-finite count
+enum { PRE_NV = 6, OBS_NV = PRE_NV + 1, POST_NV = 10 };
 
 // K8: z, optional anchor za -> per block [sum z, sum d, sum z^2, sum d^2, sum|d|, sum|za|], d = z - za
 hipError_t launch_stats_pre(const SegPlan &pl, const float *z, const float *za, float *partials, hipStream_t s);
-// K9: zhat = sum_j kappa_j out_j (j < m, slot order) -> partial non-finite counts
-hipError_t launch_observe(const SegPlan &pl, const float *const *outs, const float *kappa_dev, int m, float *zhat,
-                          float *partials, hipStream_t s);
+// K9: zhat = sum_j kappa_j out_j (j < m, slot order); per block the K8 statistics
+// of zhat against za (za may be null) followed by the count of non-finite zhat values
+hipError_t launch_observe(const SegPlan &pl, const float *const *outs, const float *kappa, int m, const float *za,
+                          float *zhat, float *partials, hipStream_t s);
 // K7: exact-step epilogue. If v: zn = z + dt*v and zn is written to zn_out; else zn is read from zn_in.
 // Copies zn to bank_slot and z to anchor_out (each when non-null). Per block:
-// [sum zn, sum (zn-za), sum (zn-z), sum zn^2, sum (zn-za)^2, sum (zn-z)^2, sum|zn-zhat|, sum|zn|, 0]
+// [sum zn, sum (zn-za), sum (zn-z), sum zn^2, sum (zn-za)^2, sum (zn-z)^2, sum|zn-zhat|, sum|zn|,
+//  sum|zn-z|, sum|z|]; entries 0, 2, 3, 5, 8, 9 are the K8 statistics of zn against the anchor z
 struct PostArgs {
   const float *z, *v, *zn_in, *za, *zhat;
   float dt;

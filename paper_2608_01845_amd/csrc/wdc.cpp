@@ -57,8 +57,9 @@ struct wdc_ctx {
   // timing
   bool timing = false;
   std::vector<TimedEvent> events;
-  double t_ms[3] = {0, 0, 0};
-  int64_t t_cnt[3] = {0, 0, 0};
+  double t_ms[WDC_T_COUNT] = {};
+  int64_t t_cnt[WDC_T_COUNT] = {};
+  double t_work[WDC_T_COUNT] = {};
 };
 
 namespace {
@@ -87,6 +88,10 @@ struct wdc_state {
   double *d_red = nullptr;
   double *h_red = nullptr;  // pinned host
   std::vector<double> n8;   // element count of each fine segment [C*8]
+  // pass-1 statistics [nseg, PRE_NV] of the latent the next step starts from,
+  // emitted by the kernel that produced it (observation or exact epilogue);
+  // only the rollout loop, which owns that latent, reads them
+  std::vector<double> pre_obs, pre_post;
   // pending pre-decision data of step k
   int pend_k = -1;
   bool pend_cand = false;   // a candidate exists (bank non-empty)
@@ -236,9 +241,11 @@ WsLayout ws_layout(const wdc_ctx *c) {
 }
 
 // ---------------------------------------------------------------- timing
+// work: algorithmic FLOPs (matrix classes) or HBM bytes (streaming classes) of the launch
 template <typename F>
-hipError_t timed(wdc_ctx *c, int cls, F &&fn) {
+hipError_t timed(wdc_ctx *c, int cls, double work, F &&fn) {
   if (!c->timing) return fn();
+  c->t_work[cls] += work;
   TimedEvent ev;
   ev.cls = cls;
   hipEventCreate(&ev.a);
@@ -270,7 +277,7 @@ wdc_status gemm(wdc_ctx *c, const void *a, int64_t lda, const void *w, const voi
   g.n = n;
   g.k = k;
   g.epi = epi;
-  HIPCHK(c, timed(c, 1, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
+  HIPCHK(c, timed(c, WDC_T_GEMM, 2.0 * m * n * k, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
   return WDC_OK;
 }
 
@@ -297,7 +304,8 @@ wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
   a.ldo = ldo;
   a.heads = c->H;
   a.hd = c->hd;
-  HIPCHK(c, timed(c, 0, [&] { return launch_attention(c->d.dtype, a, c->stream); }));
+  const double aw = 4.0 * (double)c->n * (double)c->n * c->hd * c->H;
+  HIPCHK(c, timed(c, WDC_T_ATTENTION, aw, [&] { return launch_attention(c->d.dtype, a, c->stream); }));
   return WDC_OK;
 }
 
@@ -324,8 +332,10 @@ wdc_status qkv_prep(wdc_ctx *c, const void *src, int64_t ld, int64_t row0, int64
 char *elem(wdc_ctx *c, void *base, int64_t off) { return (char *)base + off * c->esz; }
 
 wdc_status ln_mod(wdc_ctx *c, int64_t row0, int64_t rows, const float *shift, const float *scale) {
-  HIPCHK(c, launch_ln_mod(c->d.dtype, c->x + row0 * c->D, c->D, elem(c, c->h, row0 * c->D), c->D, rows, c->D, shift,
-                          scale, c->stream));
+  HIPCHK(c, timed(c, WDC_T_NORM, (double)rows * c->D * (4 + c->esz), [&] {
+    return launch_ln_mod(c->d.dtype, c->x + row0 * c->D, c->D, elem(c, c->h, row0 * c->D), c->D, rows, c->D, shift,
+                         scale, c->stream);
+  }));
   return WDC_OK;
 }
 
@@ -540,18 +550,24 @@ void log_clear(wdc_step_log *l) {
 }
 
 // Pass 1 + candidate (Eq. (2)-(5)) for step k; keeps it pending in the state.
-wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zhat, wdc_step_log *log) {
+// pre: pass-1 statistics of z [nseg, PRE_NV] already at hand, else null (computed here).
+wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zhat, wdc_step_log *log,
+                          const double *pre = nullptr) {
   wdc_ctx *c = st->ctx;
   const auto &p = c->p;
   const int nseg = st->plan.nseg();
-  const int C = c->d.lat_c;
   const float *za = st->has_anchor ? st->anchor[st->acur] : nullptr;
-  HIPCHK(c, launch_stats_pre(st->plan, z, za, st->partials, c->stream));
-  CHK(fetch(st, PRE_NV));
+  if (!pre) {
+    const double bytes = (za ? 8.0 : 4.0) * c->E;
+    HIPCHK(c, timed(c, WDC_T_STATS, bytes,
+                    [&] { return launch_stats_pre(st->plan, z, za, st->partials, c->stream); }));
+    CHK(fetch(st, PRE_NV));
+    pre = st->h_red;
+  }
   std::vector<double> sz(nseg), sd(nseg);
   double qz = 0, qd = 0, ad = 0, aa = 0;
   for (int i = 0; i < nseg; ++i) {
-    const double *r = st->h_red + i * PRE_NV;
+    const double *r = pre + i * PRE_NV;
     sz[i] = r[0];
     sd[i] = r[1];
     qz += r[2];
@@ -559,7 +575,6 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
     ad += r[4];
     aa += r[5];
   }
-  (void)C;
   summary_latent(st, sz.data(), qz, sd.data(), qd, st->has_anchor, st->s_phi);
   summary_tail(st, st->s_phi);
   const double t = t_at(k, S), tn = t_at(k + 1, S);
@@ -623,10 +638,16 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
     outs[j] = st->bank[slots[j]];
     kf[j] = (float)kap[slots[j]];
   }
-  HIPCHK(c, launch_observe(st->plan, outs, kf, nb, zhat, st->partials, c->stream));
+  const double obytes = (4.0 * nb + 4.0 + (za ? 4.0 : 0.0)) * c->E;
+  HIPCHK(c, timed(c, WDC_T_OBSERVE, obytes, [&] { return launch_observe(st->plan, outs, kf, nb, za, zhat, st->partials, c->stream); }));
   CHK(fetch(st, OBS_NV));
   double nonfinite = 0;
-  for (int i = 0; i < nseg; ++i) nonfinite += st->h_red[i];
+  st->pre_obs.resize((size_t)nseg * PRE_NV);
+  for (int i = 0; i < nseg; ++i) {
+    const double *r = st->h_red + i * OBS_NV;
+    for (int j = 0; j < PRE_NV; ++j) st->pre_obs[(size_t)i * PRE_NV + j] = r[j];
+    nonfinite += r[PRE_NV];
+  }
   st->pend_cand = true;
   st->pend_zhat = zhat;
   st->pend_support = (int)supp.size();
@@ -691,10 +712,14 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   a.has_zhat = st->pend_cand ? 1 : 0;
   a.bank_slot = st->bank[slot];
   a.anchor_out = st->anchor[st->acur ^ 1];
-  HIPCHK(c, launch_exact_post(st->plan, a, st->partials, c->stream));
+  // z and v (or zn) read, za and zhat read when present; zn, bank slot and anchor copy written
+  const double pbytes = 4.0 * c->E * (2 + a.has_anchor + a.has_zhat + (a.v ? 1 : 0) + 2);
+  HIPCHK(c, timed(c, WDC_T_EXACT_POST, pbytes,
+                  [&] { return launch_exact_post(st->plan, a, st->partials, c->stream); }));
   CHK(fetch(st, POST_NV));
   std::vector<double> sn(nseg), sdn(nseg), sdx(nseg);
   double qn = 0, qdn = 0, qdx = 0, acf = 0, an = 0;
+  st->pre_post.resize((size_t)nseg * PRE_NV);
   for (int i = 0; i < nseg; ++i) {
     const double *r = st->h_red + i * POST_NV;
     sn[i] = r[0];
@@ -705,6 +730,14 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
     qdx += r[5];
     acf += r[6];
     an += r[7];
+    // next step's pass 1: latent zn against the new anchor z
+    double *q = &st->pre_post[(size_t)i * PRE_NV];
+    q[0] = r[0];
+    q[1] = r[2];
+    q[2] = r[3];
+    q[3] = r[5];
+    q[4] = r[8];
+    q[5] = r[9];
   }
   const double E = (double)c->E;
   // counterfactual defect (Eq. (7)) and calibration (Eq. (8))
@@ -1123,7 +1156,7 @@ wdc_status wdc_dit_forward(wdc_ctx *ctx, const float *d_z, double t, const void 
 wdc_status wdc_scheduler_step(wdc_ctx *ctx, const float *d_z, const float *d_v, double t_cur, double t_next,
                               float *d_z_next, int64_t numel) {
   if (!ctx || !d_z || !d_v || !d_z_next || numel < 0) return WDC_E_ARG;
-  HIPCHK(ctx, launch_psi(d_z, d_v, (float)(t_next - t_cur), d_z_next, numel, ctx->stream));
+  HIPCHK(ctx, timed(ctx, WDC_T_PSI, 12.0 * numel, [&] { return launch_psi(d_z, d_v, (float)(t_next - t_cur), d_z_next, numel, ctx->stream); }));
   return WDC_OK;
 }
 
@@ -1181,13 +1214,15 @@ wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const
   float *zc = ctx->r_zcur, *zh = ctx->r_zhat, *zn = ctx->r_znext;
   HIPCHK(ctx, hipMemcpyAsync(zc, d_z, bytes, hipMemcpyDeviceToDevice, ctx->stream));
   wdc_step_log tmp;
+  std::vector<double> pre;  // pass-1 statistics of zc, emitted by the kernel that wrote it
   for (int k = 0; k < S; ++k) {
     wdc_step_log *lg = h_log ? &h_log[k] : &tmp;
-    CHK(surrogate_step(st, zc, k, S, zh, lg));
+    CHK(surrogate_step(st, zc, k, S, zh, lg, k > 0 ? pre.data() : nullptr));
     pre_decision(st, k, S, mode, h_forced ? h_forced[k] : 0, lg);
     if (st->pend_surrogate) {
       post_surrogate(st, lg);
       std::swap(zc, zh);
+      pre.swap(st->pre_obs);
       h_schedule[k] = 1;
     } else {
       const float *v;
@@ -1199,6 +1234,7 @@ wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const
       }
       CHK(post_exact(st, zc, v, zn, k, S, lg));
       std::swap(zc, zn);
+      pre.swap(st->pre_post);
       h_schedule[k] = 0;
     }
   }
@@ -1223,7 +1259,8 @@ wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const v
   a.ldo = ldo;
   a.heads = ctx->H;
   a.hd = ctx->hd;
-  HIPCHK(ctx, timed(ctx, 0, [&] { return launch_attention(ctx->d.dtype, a, ctx->stream); }));
+  const double aw = 4.0 * (double)n * (double)n * ctx->hd * ctx->H;
+  HIPCHK(ctx, timed(ctx, WDC_T_ATTENTION, aw, [&] { return launch_attention(ctx->d.dtype, a, ctx->stream); }));
   return WDC_OK;
 }
 
@@ -1241,14 +1278,16 @@ wdc_status wdc_set_timing(wdc_ctx *ctx, int32_t on) {
     hipEventDestroy(e.b);
   }
   ctx->events.clear();
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < WDC_T_COUNT; ++i) {
     ctx->t_ms[i] = 0;
     ctx->t_cnt[i] = 0;
+    ctx->t_work[i] = 0;
   }
   return WDC_OK;
 }
 
-wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[3], int64_t out_count[3]) {
+wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[WDC_T_COUNT], int64_t out_count[WDC_T_COUNT],
+                      double out_work[WDC_T_COUNT]) {
   if (!ctx || !out_ms || !out_count) return WDC_E_ARG;
   HIPCHK(ctx, hipStreamSynchronize(ctx->stream));
   for (auto &e : ctx->events) {
@@ -1260,9 +1299,10 @@ wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[3], int64_t out_count[3]) {
     hipEventDestroy(e.b);
   }
   ctx->events.clear();
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < WDC_T_COUNT; ++i) {
     out_ms[i] = ctx->t_ms[i];
     out_count[i] = ctx->t_cnt[i];
+    if (out_work) out_work[i] = ctx->t_work[i];
   }
   return WDC_OK;
 }

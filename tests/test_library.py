@@ -136,3 +136,13 @@ def test_state_and_workspace_sizes(wdc):
         assert lib.wdc_attn_pad(67576) % 256 == 0 and lib.wdc_attn_pad(67576) >= 67576
     finally:
         lib.wdc_destroy(h)
+
+
+def test_timing_classes_match_header(wdc):
+    src = open(os.path.join(ROOT, "include", "wdc.h")).read()
+    consts = {m.group(1).lower(): int(m.group(2)) for m in re.finditer(r"WDC_T_([A-Z_]+)\s*=\s*(\d+)", src)}
+    count = consts.pop("count")
+    from paper_2608_01845_amd import _binding
+    assert len(_binding.TIMING_CLASSES) == count
+    for name, idx in consts.items():
+        assert _binding.TIMING_CLASSES[idx] == name
