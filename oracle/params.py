@@ -47,6 +47,20 @@ class Params:
     k_init: int = 1                # mandatory-exact initialisation steps
     k_ref: int = 0                 # mandatory-exact refinement steps at the end
     tau_risk: float = 0.5
+    # Variants compared in the ablation study (Sec. 5.4, matched-budget tables).
+    # Controller "periodic": exact when k mod period == 0, otherwise the
+    # surrogate whenever it is available (periodic placement).
+    period: int = 4
+    # Surrogate construction: "lifted" (Eq. (2)-(5)) or "secant" (native latent
+    # secant: extrapolate the latest exact transition in latent space).
+    surrogate: str = "lifted"
+    # Observation: "kernel" (Eq. (5)) or "linear" (undo the RMS normalisation of
+    # the evolved latent block of the lifted state).
+    observation: str = "kernel"
+    lift_condition: bool = True      # False: no condition / phase information in the lift
+    impact_weight: bool = True       # False: w_t = 1 (no future-impact weighting, Eq. (9))
+    calibrate: bool = True           # False: eta_d stays at eta0 (no counterfactual calibration)
+    support_constraint: bool = True  # False: availability ignores retrieval support
 
 
 DEFAULTS = Params()

@@ -48,7 +48,9 @@ def local_proxy(z, z_anchor, n_s: int, q: float, q_a: float, p, d_cam: float = 0
 
 
 def sensitivity_weight(q: float, p, d_cam: float = 0.0, d_depth: float = 0.0) -> float:
-    """w_t of Eq. (9), capped at 2."""
+    """w_t of Eq. (9), capped at 2; 1 when future-impact weighting is switched off."""
+    if not p.impact_weight:
+        return 1.0
     u_cam, u_depth, u_phase = min(1.0, d_cam), min(1.0, d_depth), q
     return min(2.0, 1.0 + p.a_cam * u_cam + p.a_depth * u_depth + p.a_phase * u_phase)
 
@@ -73,9 +75,11 @@ def calibrate(eta: float, d_cf: float, proxy: float, p) -> float:
 
 def available(bank_size: int, n_s: int, support: int, finite: bool, k: int, steps: int, p) -> bool:
     """Available_t (Sec. 4.3, reliability decision): non-empty memory, anchor age
-    (consecutive surrogate commits) at most A_max, adequate support, finite
-    candidate, and the step outside the mandatory-exact initial and final phases."""
-    return (bank_size > 0 and n_s <= p.age_max and support >= p.n_min and finite
+    (consecutive surrogate commits) at most A_max, adequate support (unless the
+    support constraint is switched off), finite candidate, and the step outside
+    the mandatory-exact initial and final phases."""
+    supported = support >= p.n_min or not p.support_constraint
+    return (bank_size > 0 and n_s <= p.age_max and supported and finite
             and k >= p.k_init and k <= steps - 1 - p.k_ref)
 
 

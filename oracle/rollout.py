@@ -19,8 +19,11 @@ k = 0..S-1 (the paper's t -> t-1 is k -> k+1, q_k = t_k):
    and the surrogate count resets.
 
 Modes: "risk" (Eq. (10) as written), "forced" (decisions from a mask, with
-unsupported candidates still falling back to exact), "all_exact" and the same
-loop with F_theta replaced by recorded velocities (``replay_v``).
+unsupported candidates still falling back to exact), "periodic" (exact when
+k mod period == 0, else the surrogate when available: the periodic placement
+of the ablation study, Sec. 5.4), "all_exact", and the same loop with F_theta
+replaced by recorded velocities (``replay_denoiser``). The surrogate
+construction and the ablation switches come from the parameters.
 """
 from __future__ import annotations
 
@@ -88,7 +91,10 @@ def rollout(denoise: Callable[[np.ndarray, int, float], np.ndarray], z_T, steps:
         t, tn = t_at(k, steps), t_at(k + 1, steps)
         phi = sg.lift(z, z_a, h, t, cam_desc, p)
         bank_before = len(bank)
-        cand = sg.candidate(phi, bank, tn, q_a, q_am1, p)
+        if p.surrogate == "secant":
+            cand = sg.secant_candidate(z, z_a, bank, t, tn, q_a, q_am1, p)
+        else:
+            cand = sg.candidate(phi, bank, tn, q_a, q_am1, p, z=z)
         support = len(cand.support) if cand else 0
         finite = cand.finite if cand else False
         prox = rk.local_proxy(z, z_a, n_s, t, q_a, p)
@@ -97,6 +103,8 @@ def rollout(denoise: Callable[[np.ndarray, int, float], np.ndarray], z_T, steps:
         avail = rk.available(len(bank), n_s, support, finite, k, steps, p)
         if mode == "forced":
             take = bool(forced[k]) and avail
+        elif mode == "periodic":
+            take = k % p.period != 0 and avail
         else:
             take = rk.decide(avail, r_cand, tau)
         margin = abs(r_cand - tau) / max(abs(tau), 1e-12) if np.isfinite(tau) else np.inf
@@ -110,9 +118,11 @@ def rollout(denoise: Callable[[np.ndarray, int, float], np.ndarray], z_T, steps:
             v = np.asarray(denoise(z, k, t), dtype=np.float64)
             calls += 1
             z_next = psi(z, v, t, tn)
-            if cand is not None and support >= p.n_min and finite:
+            supported = support >= p.n_min or not p.support_constraint
+            if cand is not None and supported and finite:
                 d_cf = rk.counterfactual_defect(z_next, cand.z_hat, p.eps)
-                eta = rk.calibrate(eta, d_cf, prox.p, p)
+                if p.calibrate:
+                    eta = rk.calibrate(eta, d_cf, prox.p, p)
             R = p.lam * R
             phi_out = sg.lift(z_next, z_a, h, tn, cam_desc, p)
             slot = bank.insert(sg.Record(phi, phi_out, sg.summary(phi), sg.summary(phi_out), t, tn,

@@ -17,6 +17,17 @@ channel c with floor(j*G/T) = g, T = F*H*W. q is not part of s.
 Transition retrieval, Eq. (3); scheduler scaling and lifted evolution, Eq. (4);
 kernelized observation, Eq. (5). The lifted evolution is carried out on the
 full-size lifted state and only then summarised.
+
+Variants of the ablation study (Sec. 5.4, matched-budget tables), as read here:
+
+* linear observation: the evolved lifted state is read back linearly, by
+  undoing the RMS normalisation of its latent block:
+  z_hat = rho(z_t) * phi_hat.z, rho(x) = sqrt(mean(x^2) + eps_nu);
+* lift without condition: the camera/depth blocks are zero and retrieval
+  ignores the scheduler phase (no phase penalty, no phase compatibility test);
+* native latent secant: no lift at all; the latest exact transition
+  (z_a -> z_out, phases q_a -> q_{a-1}) is extrapolated in latent space,
+  z_hat = z_t + (q_{t-1} - q_t) / (q_{a-1} - q_a) * (z_out - z_a).
 """
 from __future__ import annotations
 
@@ -84,7 +95,8 @@ def lift(z, z_anchor, h, q: float, cam_desc, p) -> Lifted:
     z = f64(z)
     dz = np.zeros_like(z) if z_anchor is None else nu(z - f64(z_anchor), p.eps_nu)
     c = z.shape[0]
-    return Lifted(nu(z, p.eps_nu), dz, f64(cam_desc), np.zeros(G_CAM), float(q),
+    cam = f64(cam_desc) if p.lift_condition else np.zeros(G_CAM)
+    return Lifted(nu(z, p.eps_nu), dz, cam, np.zeros(G_CAM), float(q),
                   np.zeros(c * G_H) if h is None else f64(h))
 
 
@@ -168,9 +180,11 @@ def scheduler_scale(t_cur: float, t_next: float, q_a: float, q_am1: float, p) ->
     return float(np.clip(abs(t_next - t_cur) / (abs(q_am1 - q_a) + p.eps), p.alpha_min, p.alpha_max))
 
 
-def candidate(phi: Lifted, bank: Bank, t_next: float, q_a: float, q_am1: float, p) -> Optional[Candidate]:
+def candidate(phi: Lifted, bank: Bank, t_next: float, q_a: float, q_am1: float, p,
+              z=None) -> Optional[Candidate]:
     """G_t(z_t, H_t): retrieval (Eq. (3)), lifted evolution (Eq. (4)) and
-    kernelized observation (Eq. (5)). None when the bank is empty."""
+    kernelized observation (Eq. (5)). None when the bank is empty. ``z`` (the
+    current latent) is needed only by the linear observation."""
     recs = bank.records()
     if not recs:
         return None
@@ -178,8 +192,12 @@ def candidate(phi: Lifted, bank: Bank, t_next: float, q_a: float, q_am1: float, 
     slots = [i for i, _ in recs]
     sims_in = np.array([sim(s_t, r.s_in) for _, r in recs])
     dq = np.array([phi.q - r.q_in for _, r in recs])
-    logits = sims_in - p.gamma_q * dq ** 2
-    supp = [j for j in range(len(recs)) if sims_in[j] >= p.theta_sim and abs(dq[j]) <= p.theta_q]
+    if p.lift_condition:
+        logits = sims_in - p.gamma_q * dq ** 2
+        supp = [j for j in range(len(recs)) if sims_in[j] >= p.theta_sim and abs(dq[j]) <= p.theta_q]
+    else:
+        logits = sims_in.copy()
+        supp = [j for j in range(len(recs)) if sims_in[j] >= p.theta_sim]
     pi = np.zeros(len(recs))
     if supp:
         pi[supp] = softmax(logits[supp] / p.tau_in)
@@ -188,9 +206,34 @@ def candidate(phi: Lifted, bank: Bank, t_next: float, q_a: float, q_am1: float, 
     for j in supp:
         phi_hat = phi_hat.axpy(alpha * pi[j], recs[j][1].phi_out - recs[j][1].phi_in)
     s_hat = summary(phi_hat)
-    kappa = softmax(np.array([sim(s_hat, r.s_out) for _, r in recs]) / p.tau_obs)
-    z_hat = np.zeros_like(recs[0][1].z_out, dtype=np.float64)
-    for j, (_, r) in enumerate(recs):
-        z_hat = z_hat + kappa[j] * f64(r.z_out)
+    if p.observation == "linear":
+        zc = f64(z)
+        kappa = np.zeros(len(recs))
+        z_hat = np.sqrt(np.mean(zc * zc) + p.eps_nu) * phi_hat.z
+    else:
+        kappa = softmax(np.array([sim(s_hat, r.s_out) for _, r in recs]) / p.tau_obs)
+        z_hat = np.zeros_like(recs[0][1].z_out, dtype=np.float64)
+        for j, (_, r) in enumerate(recs):
+            z_hat = z_hat + kappa[j] * f64(r.z_out)
     return Candidate([slots[j] for j in supp], sims_in, logits, pi, alpha, s_hat, kappa, z_hat,
+                     bool(np.all(np.isfinite(z_hat))), slots)
+
+
+def secant_candidate(z, z_anchor, bank: Bank, t_cur: float, t_next: float, q_a: float, q_am1: float,
+                     p) -> Optional[Candidate]:
+    """Native latent secant: the latest exact transition z_a -> z_out, taken over
+    the phase interval q_a -> q_{a-1}, extrapolated from z_t over q_t -> q_{t-1}.
+    None when no exact transition has been recorded."""
+    recs = bank.records()
+    if not recs or z_anchor is None:
+        return None
+    latest = (bank.inserts - 1) % bank.capacity
+    slots = [i for i, _ in recs]
+    j = slots.index(latest)
+    ratio = (t_next - t_cur) / (q_am1 - q_a)
+    z_hat = f64(z) + ratio * (f64(bank.slots[latest].z_out) - f64(z_anchor))
+    n = len(recs)
+    pi = np.zeros(n)
+    pi[j] = 1.0
+    return Candidate([latest], np.zeros(n), np.zeros(n), pi, ratio, np.zeros(S_DIM), np.zeros(n), z_hat,
                      bool(np.all(np.isfinite(z_hat))), slots)
