@@ -54,8 +54,23 @@ enum { WDC_F32 = 0, WDC_BF16 = 1 };
 /* Rollout modes. RISK: Eq. (10) as written. FORCED: the decision of step k is
  * h_forced[k] (1 = surrogate), still falling back to exact when the candidate is
  * unsupported (Sec. 4.3, last sentence of "Reliability Decision"). ALL_EXACT:
- * every step exact; candidates are still built and logged. */
-enum { WDC_MODE_RISK = 0, WDC_MODE_FORCED = 1, WDC_MODE_ALL_EXACT = 2 };
+ * every step exact; candidates are still built and logged. PERIODIC: exact when
+ * k mod params.period == 0, otherwise the surrogate whenever it is available
+ * (the periodic placement of the ablation study, Sec. 5.4). */
+enum { WDC_MODE_RISK = 0, WDC_MODE_FORCED = 1, WDC_MODE_ALL_EXACT = 2, WDC_MODE_PERIODIC = 3 };
+
+/* Surrogate construction (wdc_params.surrogate). LIFTED: Eq. (2)-(5). SECANT:
+ * native latent secant of the ablation study (Sec. 5.4): the latest exact
+ * transition z_a -> z_out over phases q_a -> q_{a-1} extrapolated from z_t,
+ * z_hat = z_t + (q_{t-1} - q_t) / (q_{a-1} - q_a) * (z_out - z_a). */
+enum { WDC_SURROGATE_LIFTED = 0, WDC_SURROGATE_SECANT = 1 };
+
+/* Observation (wdc_params.observation). KERNEL: Eq. (5). LINEAR: the evolved
+ * lifted state is read back linearly by undoing the RMS normalisation of its
+ * latent block, z_hat = rho(z_t) * (nu(z_t) + alpha * sum_{i in N_t} pi_i
+ * (nu(z_i^out) - nu(z_i^in))), rho(x) = sqrt(mean(x^2) + eps_nu); the state then
+ * also keeps each record's input latent. */
+enum { WDC_OBS_KERNEL = 0, WDC_OBS_LINEAR = 1 };
 
 /* Phases of wdc_risk_update. */
 enum { WDC_PRE_DECISION = 0, WDC_POST_EXACT = 1, WDC_POST_SURROGATE = 2 };
@@ -96,6 +111,15 @@ typedef struct {
   double eta0, beta_d, eta_min, eta_max;      /* Eq. (8) */
   double a_cam, a_depth, a_phase, lam, r0;    /* Eq. (9) */
   double tau_risk;                            /* Eq. (10) */
+  /* Variants of the ablation study (Sec. 5.4); the defaults are the full method. */
+  int32_t period;             /* WDC_MODE_PERIODIC: exact when k mod period == 0 (>= 1) */
+  int32_t surrogate;          /* WDC_SURROGATE_* */
+  int32_t observation;        /* WDC_OBS_* */
+  int32_t lift_condition;     /* 0: camera/depth blocks zero, retrieval without the phase terms of Eq. (3) */
+  int32_t impact_weight;      /* 0: w_t = 1 (no future-impact weighting, Eq. (9)) */
+  int32_t calibrate;          /* 0: eta_d stays at eta0 (no counterfactual calibration, Eq. (8)) */
+  int32_t support_constraint; /* 0: availability does not require |N_t| >= n_min */
+  int32_t pad_;
 } wdc_params;
 
 #define WDC_MAX_BANK 8

@@ -17,7 +17,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libwdc.so")
 
 WDC_F32, WDC_BF16 = 0, 1
-MODE_RISK, MODE_FORCED, MODE_ALL_EXACT = 0, 1, 2
+MODE_RISK, MODE_FORCED, MODE_ALL_EXACT, MODE_PERIODIC = 0, 1, 2, 3
+SURROGATE_LIFTED, SURROGATE_SECANT = 0, 1
+OBS_KERNEL, OBS_LINEAR = 0, 1
 PRE_DECISION, POST_EXACT, POST_SURROGATE = 0, 1, 2
 MAX_BANK = 8
 # kernel timing classes, in the order of the WDC_T_* constants
@@ -52,7 +54,9 @@ class Params(C.Structure):
                 ("k_ref", C.c_int32)] + [(n, C.c_double) for n in (
                     "theta_sim", "theta_q", "tau_in", "tau_obs", "gamma_q", "alpha_min", "alpha_max", "eps", "eps_nu",
                     "w_z", "w_age", "w_phase", "w_cam", "w_depth", "eta0", "beta_d", "eta_min", "eta_max",
-                    "a_cam", "a_depth", "a_phase", "lam", "r0", "tau_risk")]
+                    "a_cam", "a_depth", "a_phase", "lam", "r0", "tau_risk")] + [(n, C.c_int32) for n in (
+                    "period", "surrogate", "observation", "lift_condition", "impact_weight", "calibrate",
+                    "support_constraint", "pad_")]
 
 
 class StepLog(C.Structure):

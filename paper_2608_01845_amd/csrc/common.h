@@ -6,7 +6,7 @@
 #include <stdint.h>
 #include <string>
 
-#define WDC_MAXB 8  // largest bank capacity the kernels take (matches WDC_MAX_BANK)
+#define WDC_MAXB 17  // most latents one observation combine reads: 2 per bank slot (8) + the current one
 
 namespace wdc {
 
@@ -179,13 +179,13 @@ hipError_t launch_stats_pre(const SegPlan &pl, const float *z, const float *za, 
 hipError_t launch_observe(const SegPlan &pl, const float *const *outs, const float *kappa, int m, const float *za,
                           float *zhat, float *partials, hipStream_t s);
 // K7: exact-step epilogue. If v: zn = z + dt*v and zn is written to zn_out; else zn is read from zn_in.
-// Copies zn to bank_slot and z to anchor_out (each when non-null). Per block:
+// Copies zn to bank_slot and z to anchor_out and in_slot (each when non-null). Per block:
 // [sum zn, sum (zn-za), sum (zn-z), sum zn^2, sum (zn-za)^2, sum (zn-z)^2, sum|zn-zhat|, sum|zn|,
 //  sum|zn-z|, sum|z|]; entries 0, 2, 3, 5, 8, 9 are the K8 statistics of zn against the anchor z
 struct PostArgs {
   const float *z, *v, *zn_in, *za, *zhat;
   float dt;
-  float *zn_out, *bank_slot, *anchor_out;
+  float *zn_out, *bank_slot, *anchor_out, *in_slot;
   int has_anchor, has_zhat;
 };
 hipError_t launch_exact_post(const SegPlan &pl, const PostArgs &a, float *partials, hipStream_t s);

@@ -182,6 +182,7 @@ struct PostOp {
     }
     if (a.bank_slot) stv<W>(a.bank_slot, i, xn);
     if (a.anchor_out) stv<W>(a.anchor_out, i, x);
+    if (a.in_slot) stv<W>(a.in_slot, i, x);
     const Vf<W> za = a.has_anchor ? ldv<W>(a.za, i) : zeros<W>();
     const Vf<W> zh = a.has_zhat ? ldv<W>(a.zhat, i) : zeros<W>();
 #pragma unroll
@@ -278,7 +279,7 @@ hipError_t launch_observe(const SegPlan &pl, const float *const *outs, const flo
 hipError_t launch_exact_post(const SegPlan &pl, const PostArgs &a, float *partials, hipStream_t s) {
   SegPlan p = pl;
   p.vec = al16(a.z) && al16(a.v) && al16(a.zn_in) && al16(a.za) && al16(a.zhat) && al16(a.zn_out) &&
-          al16(a.bank_slot) && al16(a.anchor_out);
+          al16(a.bank_slot) && al16(a.anchor_out) && al16(a.in_slot);
   hipLaunchKernelGGL(k_exact_post, dim3(p.nblocks()), dim3(kThreads), 0, s, p, PostOp{a}, partials);
   return hipGetLastError();
 }

@@ -66,6 +66,7 @@ namespace {
 struct Record {
   double s_in[S_DIM], s_out[S_DIM];
   double q_in, q_out;
+  double rho_in, rho_out;  // sqrt(mean(z^2) + eps_nu) of the input and output latents
 };
 }  // namespace
 
@@ -77,6 +78,7 @@ struct wdc_state {
   bool has_anchor = false;
   double q_a = 0, q_am1 = 0;
   float *bank[WDC_MAX_BANK] = {};
+  float *bank_in[WDC_MAX_BANK] = {};  // input latents of the records (linear observation only)
   Record rec[WDC_MAX_BANK];
   bool filled[WDC_MAX_BANK] = {};
   int inserts = 0;
@@ -99,6 +101,7 @@ struct wdc_state {
   int pend_support = 0;
   bool pend_finite = false;
   double s_phi[S_DIM];
+  double rho_cur = 0;  // sqrt(mean(z_k^2) + eps_nu) of the pending step's latent
   double proxy = 0, r_cand = 0, d_hat = 0, wgt = 1, margin = 0;
   bool pend_avail = false, pend_decided = false, pend_surrogate = false;
 };
@@ -529,7 +532,8 @@ void summary_latent(const wdc_state *st, const double *segsum_z, double sq_z, co
 void summary_tail(const wdc_state *st, double *s) {
   const int o = st->ctx->d.lat_c * (G8 + G4);
   for (int i = 0; i < 32; ++i) s[o + i] = st->hsum[i];
-  for (int i = 0; i < GCAM; ++i) s[o + 32 + i] = st->cam[i];
+  const bool cond = st->ctx->p.lift_condition != 0;
+  for (int i = 0; i < GCAM; ++i) s[o + 32 + i] = cond ? st->cam[i] : 0.0;
   for (int i = 0; i < GCAM; ++i) s[o + 48 + i] = 0.0;  // depth: unavailable
 }
 
@@ -577,6 +581,7 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
   }
   summary_latent(st, sz.data(), qz, sd.data(), qd, st->has_anchor, st->s_phi);
   summary_tail(st, st->s_phi);
+  st->rho_cur = std::sqrt(qz / (double)c->E + p.eps_nu);
   const double t = t_at(k, S), tn = t_at(k + 1, S);
   // risk proxy terms that only need pass-1 statistics (Eq. (6))
   double dz = 0, dph = 0;
@@ -606,40 +611,76 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
   nb = (int)slots.size();
   log->bank = nb;
   if (nb == 0) return WDC_OK;
-  // retrieval (Eq. (3))
-  double sims[WDC_MAX_BANK] = {}, logit[WDC_MAX_BANK] = {}, pi[WDC_MAX_BANK] = {}, kap[WDC_MAX_BANK] = {};
-  std::vector<int> supp, all;
+  double sims[WDC_MAX_BANK] = {}, pi[WDC_MAX_BANK] = {}, kap[WDC_MAX_BANK] = {};
+  double alpha = 0;
+  int support = 0;
+  // linear combination zhat = sum_j coef_j * src_j evaluated by the observation kernel
+  const float *src[WDC_MAXB];
+  float coef[WDC_MAXB];
+  int m = 0;
+  if (p.surrogate == WDC_SURROGATE_SECANT) {
+    // native latent secant: the latest exact transition anchor -> bank[latest]
+    const int latest = (st->inserts - 1) % p.bank_capacity;
+    alpha = (tn - t) / (st->q_am1 - st->q_a);
+    src[0] = z;
+    src[1] = st->bank[latest];
+    src[2] = za;
+    coef[0] = 1.0f;
+    coef[1] = (float)alpha;
+    coef[2] = (float)-alpha;
+    m = 3;
+    pi[latest] = 1.0;
+    support = 1;
+  } else {
+    // retrieval (Eq. (3)); without condition information the phase terms drop out
+    double logit[WDC_MAX_BANK] = {};
+    std::vector<int> supp, all;
+    for (int i : slots) {
+      sims[i] = cosine(st->s_phi, st->rec[i].s_in);
+      const double dq = t - st->rec[i].q_in;
+      const bool cond = p.lift_condition != 0;
+      logit[i] = (sims[i] - (cond ? p.gamma_q * dq * dq : 0.0)) / p.tau_in;
+      if (sims[i] >= p.theta_sim && (!cond || std::fabs(dq) <= p.theta_q)) supp.push_back(i);
+      all.push_back(i);
+    }
+    if (!supp.empty()) softmax(logit, supp, pi);
+    support = (int)supp.size();
+    // scheduler scaling and lifted evolution (Eq. (4))
+    alpha = std::fabs(tn - t) / (std::fabs(st->q_am1 - st->q_a) + p.eps);
+    alpha = std::min(std::max(alpha, p.alpha_min), p.alpha_max);
+    if (p.observation == WDC_OBS_LINEAR) {
+      // rho_t * (nu(z_t) + alpha * sum pi_i (nu(z_i^out) - nu(z_i^in)))
+      src[m] = z;
+      coef[m++] = 1.0f;
+      for (int i : supp) {
+        src[m] = st->bank[i];
+        coef[m++] = (float)(alpha * pi[i] * st->rho_cur / st->rec[i].rho_out);
+        src[m] = st->bank_in[i];
+        coef[m++] = (float)(-alpha * pi[i] * st->rho_cur / st->rec[i].rho_in);
+      }
+    } else {
+      // summary-space evolution (s is linear), then kernelized observation over
+      // the whole bank (Eq. (5))
+      double shat[S_DIM];
+      for (int j = 0; j < S_DIM; ++j) {
+        double acc = 0;
+        for (int i : supp) acc += pi[i] * (st->rec[i].s_out[j] - st->rec[i].s_in[j]);
+        shat[j] = st->s_phi[j] + alpha * acc;
+      }
+      double ks[WDC_MAX_BANK] = {};
+      for (int i : slots) ks[i] = cosine(shat, st->rec[i].s_out) / p.tau_obs;
+      softmax(ks, all, kap);
+      for (int i : slots) {
+        src[m] = st->bank[i];
+        coef[m++] = (float)kap[i];
+      }
+    }
+  }
   double simm = INFINITY;
-  for (int i : slots) {
-    sims[i] = cosine(st->s_phi, st->rec[i].s_in);
-    const double dq = t - st->rec[i].q_in;
-    logit[i] = (sims[i] - p.gamma_q * dq * dq) / p.tau_in;
-    if (sims[i] >= p.theta_sim && std::fabs(dq) <= p.theta_q) supp.push_back(i);
-    all.push_back(i);
-    simm = std::min(simm, std::fabs(sims[i] - p.theta_sim));
-  }
-  if (!supp.empty()) softmax(logit, supp, pi);
-  // scheduler scaling and lifted evolution in summary space (Eq. (4); s is linear)
-  double alpha = std::fabs(tn - t) / (std::fabs(st->q_am1 - st->q_a) + p.eps);
-  alpha = std::min(std::max(alpha, p.alpha_min), p.alpha_max);
-  double shat[S_DIM];
-  for (int j = 0; j < S_DIM; ++j) {
-    double acc = 0;
-    for (int i : supp) acc += pi[i] * (st->rec[i].s_out[j] - st->rec[i].s_in[j]);
-    shat[j] = st->s_phi[j] + alpha * acc;
-  }
-  // kernelized observation over the whole bank (Eq. (5))
-  double ks[WDC_MAX_BANK] = {};
-  for (int i : slots) ks[i] = cosine(shat, st->rec[i].s_out) / p.tau_obs;
-  softmax(ks, all, kap);
-  const float *outs[WDC_MAX_BANK];
-  float kf[WDC_MAX_BANK];
-  for (int j = 0; j < nb; ++j) {
-    outs[j] = st->bank[slots[j]];
-    kf[j] = (float)kap[slots[j]];
-  }
-  const double obytes = (4.0 * nb + 4.0 + (za ? 4.0 : 0.0)) * c->E;
-  HIPCHK(c, timed(c, WDC_T_OBSERVE, obytes, [&] { return launch_observe(st->plan, outs, kf, nb, za, zhat, st->partials, c->stream); }));
+  for (int i : slots) simm = std::min(simm, std::fabs(sims[i] - p.theta_sim));
+  const double obytes = (4.0 * m + 4.0 + (za ? 4.0 : 0.0)) * c->E;
+  HIPCHK(c, timed(c, WDC_T_OBSERVE, obytes,
+                  [&] { return launch_observe(st->plan, src, coef, m, za, zhat, st->partials, c->stream); }));
   CHK(fetch(st, OBS_NV));
   double nonfinite = 0;
   st->pre_obs.resize((size_t)nseg * PRE_NV);
@@ -650,7 +691,7 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
   }
   st->pend_cand = true;
   st->pend_zhat = zhat;
-  st->pend_support = (int)supp.size();
+  st->pend_support = support;
   st->pend_finite = nonfinite == 0;
   log->support = st->pend_support;
   log->finite = st->pend_finite;
@@ -668,18 +709,22 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
 void pre_decision(wdc_state *st, int k, int S, int mode, int forced, wdc_step_log *log) {
   const auto &p = st->ctx->p;
   const double t = t_at(k, S);
-  const double w = std::min(2.0, 1.0 + p.a_phase * t);  // camera / depth sensitivity: static (0)
+  // camera / depth sensitivity: static (0)
+  const double w = p.impact_weight ? std::min(2.0, 1.0 + p.a_phase * t) : 1.0;
   st->wgt = w;
   st->d_hat = st->eta * st->proxy;
   st->r_cand = p.lam * st->R + w * st->d_hat;
   int nb = 0;
   for (int i = 0; i < p.bank_capacity; ++i) nb += st->filled[i];
-  const bool avail = nb > 0 && st->n_s <= p.age_max && st->pend_support >= p.n_min && st->pend_finite &&
-                     k >= p.k_init && k <= S - 1 - p.k_ref;
+  const bool supported = st->pend_support >= p.n_min || !p.support_constraint;
+  const bool avail = nb > 0 && st->n_s <= p.age_max && supported && st->pend_finite && k >= p.k_init &&
+                     k <= S - 1 - p.k_ref;
   const double tau = mode == WDC_MODE_ALL_EXACT ? -INFINITY : p.tau_risk;
   bool take;
   if (mode == WDC_MODE_FORCED)
     take = forced && avail;
+  else if (mode == WDC_MODE_PERIODIC)
+    take = k % p.period != 0 && avail;
   else
     take = avail && st->r_cand <= tau;
   st->pend_avail = avail;
@@ -700,7 +745,7 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   const int nseg = st->plan.nseg();
   const int slot = st->inserts % p.bank_capacity;
   const double t = t_at(k, S), tn = t_at(k + 1, S);
-  PostArgs a;
+  PostArgs a{};
   a.z = z;
   a.v = v;
   a.zn_in = zn;
@@ -712,8 +757,9 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   a.has_zhat = st->pend_cand ? 1 : 0;
   a.bank_slot = st->bank[slot];
   a.anchor_out = st->anchor[st->acur ^ 1];
+  a.in_slot = st->bank_in[slot];  // null unless the linear observation keeps record inputs
   // z and v (or zn) read, za and zhat read when present; zn, bank slot and anchor copy written
-  const double pbytes = 4.0 * c->E * (2 + a.has_anchor + a.has_zhat + (a.v ? 1 : 0) + 2);
+  const double pbytes = 4.0 * c->E * (2 + a.has_anchor + a.has_zhat + (a.v ? 1 : 0) + 2 + (a.in_slot ? 1 : 0));
   HIPCHK(c, timed(c, WDC_T_EXACT_POST, pbytes,
                   [&] { return launch_exact_post(st->plan, a, st->partials, c->stream); }));
   CHK(fetch(st, POST_NV));
@@ -742,10 +788,13 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   const double E = (double)c->E;
   // counterfactual defect (Eq. (7)) and calibration (Eq. (8))
   double dcf = NAN;
-  if (st->pend_cand && st->pend_support >= p.n_min && st->pend_finite) {
+  const bool supported = st->pend_support >= p.n_min || !p.support_constraint;
+  if (st->pend_cand && supported && st->pend_finite) {
     dcf = (acf / E) / (an / E + p.eps);
-    double e = p.beta_d * st->eta + (1.0 - p.beta_d) * dcf / (st->proxy + p.eps);
-    st->eta = std::min(std::max(e, p.eta_min), p.eta_max);
+    if (p.calibrate) {
+      double e = p.beta_d * st->eta + (1.0 - p.beta_d) * dcf / (st->proxy + p.eps);
+      st->eta = std::min(std::max(e, p.eta_min), p.eta_max);
+    }
   }
   st->R = p.lam * st->R;
   // record: both lifted states under the pre-insertion anchor and history
@@ -755,6 +804,8 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   summary_tail(st, r.s_out);
   r.q_in = t;
   r.q_out = tn;
+  r.rho_in = st->rho_cur;
+  r.rho_out = std::sqrt(qn / E + p.eps_nu);
   st->filled[slot] = true;
   st->inserts++;
   // history summary h = P_2(nu(zn - z)) of this transition
@@ -862,6 +913,13 @@ void wdc_params_default(wdc_params *p) {
   p->lam = 0.8;
   p->r0 = 0.0;
   p->tau_risk = 0.5;
+  p->period = 4;
+  p->surrogate = WDC_SURROGATE_LIFTED;
+  p->observation = WDC_OBS_KERNEL;
+  p->lift_condition = 1;
+  p->impact_weight = 1;
+  p->calibrate = 1;
+  p->support_constraint = 1;
 }
 
 const char *wdc_last_error(const wdc_ctx *ctx) { return ctx ? ctx->err.c_str() : g_create_err.c_str(); }
@@ -914,6 +972,12 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
     wdc_params_default(&c->p);
   if (c->p.bank_capacity < 1 || c->p.bank_capacity > WDC_MAX_BANK) {
     g_create_err = "bank_capacity out of range";
+    delete c;
+    return WDC_E_ARG;
+  }
+  if (c->p.period < 1 || (c->p.surrogate != WDC_SURROGATE_LIFTED && c->p.surrogate != WDC_SURROGATE_SECANT) ||
+      (c->p.observation != WDC_OBS_KERNEL && c->p.observation != WDC_OBS_LINEAR)) {
+    g_create_err = "period, surrogate or observation out of range";
     delete c;
     return WDC_E_ARG;
   }
@@ -1050,13 +1114,18 @@ wdc_status wdc_bind_workspace(wdc_ctx *ctx, void *d_ws, size_t bytes) {
   return WDC_OK;
 }
 
+// anchor double buffer, bank outputs, and bank inputs for the linear observation
+static int n_latents(const wdc_ctx *ctx) {
+  return 2 + ctx->p.bank_capacity * (ctx->p.observation == WDC_OBS_LINEAR ? 2 : 1);
+}
+
 size_t wdc_state_bytes(const wdc_ctx *ctx) {
   if (!ctx) return 0;
   SegPlan pl = make_seg_plan(ctx->d.lat_c, ctx->T, G8);
   size_t lat = (((size_t)ctx->E * 4 + 255) / 256) * 256;
   size_t part = (((size_t)pl.nblocks() * POST_NV * 4 + 255) / 256) * 256;
   size_t red = (((size_t)pl.nseg() * POST_NV * 8 + 255) / 256) * 256;
-  return lat * (2 + ctx->p.bank_capacity) + part + red;
+  return lat * n_latents(ctx) + part + red;
 }
 
 wdc_status wdc_state_create(wdc_ctx *ctx, void *d_mem, size_t bytes, wdc_state **out) {
@@ -1077,7 +1146,10 @@ wdc_status wdc_state_create(wdc_ctx *ctx, void *d_mem, size_t bytes, wdc_state *
   st->anchor[0] = (float *)b;
   st->anchor[1] = (float *)(b + lat);
   for (int i = 0; i < ctx->p.bank_capacity; ++i) st->bank[i] = (float *)(b + lat * (2 + i));
-  size_t o = lat * (2 + ctx->p.bank_capacity);
+  if (ctx->p.observation == WDC_OBS_LINEAR)
+    for (int i = 0; i < ctx->p.bank_capacity; ++i)
+      st->bank_in[i] = (float *)(b + lat * (2 + ctx->p.bank_capacity + i));
+  size_t o = lat * n_latents(ctx);
   st->partials = (float *)(b + o);
   o += (((size_t)st->plan.nblocks() * POST_NV * 4 + 255) / 256) * 256;
   st->d_red = (double *)(b + o);
@@ -1193,7 +1265,7 @@ wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const
                        const void *d_cam, int32_t mode, const uint8_t *h_forced, const float *d_replay_v,
                        uint8_t *h_schedule, wdc_step_log *h_log) {
   if (!ctx || !st || st->ctx != ctx || !d_z || S < 1 || !h_schedule) return WDC_E_ARG;
-  if (mode < WDC_MODE_RISK || mode > WDC_MODE_ALL_EXACT || (mode == WDC_MODE_FORCED && !h_forced)) return WDC_E_ARG;
+  if (mode < WDC_MODE_RISK || mode > WDC_MODE_PERIODIC || (mode == WDC_MODE_FORCED && !h_forced)) return WDC_E_ARG;
   CHK(need_ws(ctx));
   if (!d_replay_v) {
     CHK(need_w(ctx));

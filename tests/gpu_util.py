@@ -36,6 +36,23 @@ def small_cfg(dtype="bf16", head_dim=64, **kw):
     return synth.ModelConfig(**base)
 
 
+def wdc_params(p):
+    """The library's parameter struct holding the oracle parameters ``p``."""
+    from dataclasses import fields
+    import paper_2608_01845_amd as wdc
+    codes = {"surrogate": {"lifted": wdc.SURROGATE_LIFTED, "secant": wdc.SURROGATE_SECANT},
+             "observation": {"kernel": wdc.OBS_KERNEL, "linear": wdc.OBS_LINEAR}}
+    out = wdc.default_params()
+    for f in fields(p):
+        v = getattr(p, f.name)
+        if f.name in codes:
+            v = codes[f.name][v]
+        elif isinstance(v, bool):
+            v = int(v)
+        setattr(out, f.name, v)
+    return out
+
+
 def context(cfg, weights=True, params=None):
     torch = torch_cuda()
     import paper_2608_01845_amd as wdc

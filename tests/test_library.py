@@ -85,6 +85,35 @@ def test_param_defaults_match_oracle_readings(wdc):
                "r0": "r0", "tau_risk": "tau_risk"}
     for c_name, o_name in mapping.items():
         assert getattr(p, c_name) == o[o_name], c_name
+    # ablation variants: the defaults are the full method
+    assert p.period == o["period"]
+    assert (p.surrogate, o["surrogate"]) == (wdc.SURROGATE_LIFTED, "lifted")
+    assert (p.observation, o["observation"]) == (wdc.OBS_KERNEL, "kernel")
+    for name in ("lift_condition", "impact_weight", "calibrate", "support_constraint"):
+        assert p.__getattribute__(name) == int(o[name]) == 1, name
+
+
+def test_params_struct_mirrors_oracle_fields(wdc):
+    """Every oracle parameter has a field of the same name in wdc_params."""
+    from dataclasses import fields
+    names = {f[0] for f in wdc.Params._fields_}
+    for f in fields(oparams.Params):
+        assert f.name in names, f.name
+    src = open(os.path.join(ROOT, "include", "wdc.h")).read()
+    body = src[src.index("typedef struct {\n  int32_t bank_capacity;"):src.index("} wdc_params;")]
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    declared = re.findall(r"\b([a-z_0-9]+)\s*[,;]", body)
+    assert declared == [f[0] for f in wdc.Params._fields_]
+
+
+def test_create_rejects_bad_variant_params(wdc):
+    cfg = synth.get_config("tiny")
+    for bad in (dict(period=0), dict(surrogate=2), dict(observation=-1)):
+        lib = wdc.load()
+        d = wdc.desc_from_config(cfg)
+        p = wdc.default_params(**bad)
+        h = C.c_void_p()
+        assert lib.wdc_create(C.byref(d), C.byref(p), None, C.byref(h)) == 1, bad
 
 
 def test_create_rejects_bad_descriptors(wdc):
