@@ -31,7 +31,8 @@ PEAK_HBM_GBS = 8000.0
 # (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, scale factors from a 1 GiB device
 # copy; profiles/attention_13b_hbm_traffic.md). Valid only for the kernel
 # version named here; set to None whenever that kernel changes.
-MEASURED_TRAFFIC = {"k_attn_bf16_pp<128>": 8.317e9}
+MEASURED_TRAFFIC = {"k_attn_bf16_pp4<128>": None}
+ATTN_KERNEL = "k_attn_bf16_pp4<128>"
 METRIC = "DiT fwd TFLOP/s (% bf16 MFMA peak) + denoising steps/s at 13B shape"
 
 
@@ -259,11 +260,11 @@ def main():
                     "gemm_ms_total": round(gemm_ms, 1), "gemm_launches": gemm_n,
                     "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None,
                     "layernorm_modulate": hbm_entry(norm_ms, norm_n, norm_work)},
-        "roofline": {"bound": "mfma", "kernel": "k_attn_bf16_pp<128>",
+        "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL,
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
-                     "traffic": MEASURED_TRAFFIC.get("k_attn_bf16_pp<128>") if args.workload == "13b" else None,
+                     "traffic": MEASURED_TRAFFIC.get(ATTN_KERNEL) if args.workload == "13b" else None,
                      "traffic_unit": "bytes per launch"},
     }
     del ctx, st, z, zbuf, zhat, v, cond, text, cam

@@ -728,6 +728,179 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp(AttnArgs a) {
   }
 }
 
+// Ping-pong kernel with four K and four V^T buffers: group A issues the loads
+// of K_{t+3} and V_{t+2} in step t, two steps before they are read, and at the
+// end of step t waits only for the loads of step t-1 (a partial vmcnt), so a
+// tile load has two full steps to land. The step loop is unrolled by four so
+// every LDS fragment address is a per-lane register plus an immediate offset.
+// Buffer reuse: K_{t+3} overwrites K_{t-1}, last read in the matrix phases of
+// step t-2; V_{t+2} overwrites V_{t-2}, last read in step t-2; both end at a
+// barrier before step t starts. Group B's prologue reads K_0 while group A's
+// first step fills buffers 3 (K) and 2 (V).
+template <int HD>
+__device__ __forceinline__ void pp4_wait(int n_outstanding) {
+  constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
+  static_assert(KS + VS < 16, "vmcnt immediate");
+  if (n_outstanding == KS + VS)
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | (KS + VS));
+  else if (n_outstanding == VS)
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | VS);
+  else
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+}
+
+template <int HD>
+__global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
+  constexpr int QB = 256;                  // 8 waves x 32 queries
+  constexpr int NB = 4;                    // K buffers and V^T buffers
+  constexpr int K_BYTES = KV * HD * 2;
+  constexpr int V_BASE = NB * K_BYTES;     // V^T buffers follow the K buffers
+  using TL = TileLoad<HD>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+
+  int h = blockIdx.y, qb = blockIdx.x;
+  if (a.xcd_order) {
+    const int id = blockIdx.x + blockIdx.y * gridDim.x;
+    const int li = id >> 3;
+    h = (id & 7) + 8 * (li / gridDim.x);
+    qb = li % gridDim.x;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool grp_a = wid < 4;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int64_t qbase = (int64_t)qb * QB + wid * 32;
+  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
+
+  bf16x8 qf[HD / 16];
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) qf[s] = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
+
+  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const int lw = wid & 3;
+  const TileLoad<HD> tl(lw, lane, a.n_pad);
+  int kro[HD / 16];
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
+  int vro[4];                              // V^T fragment offsets, V region base folded in
+#pragma unroll
+  for (int j = 0; j < 4; ++j) vro[j] = V_BASE + vslot(lr, 2 * j + lg);
+
+  const int ntiles = (int)((a.n + KV - 1) / KV);
+  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
+  auto load_k = [&](int b, int tile) {
+#pragma unroll
+    for (int i = 0; i < TL::K_STRIPES; ++i)
+      lds_load16(kdesc, smem + b * K_BYTES + lw * 1024 + i * 4096, tl.kvo, tile * KV * HD * 2 + i * 4096);
+  };
+  auto load_v = [&](int b, int tile) {
+#pragma unroll
+    for (int i = 0; i < TL::V_STRIPES; ++i)
+      lds_load16(vdesc, smem + V_BASE + b * K_BYTES + lw * 1024 + i * 4096, tl.vvo,
+                 tile * KV * 2 + i * 32 * (int)a.n_pad * 2);
+  };
+
+  if (grp_a) {
+    load_k(0, 0);
+    load_v(0, 0);
+    if (ntiles > 1) {
+      load_k(1, 1);
+      load_v(1, 1);
+    }
+    if (ntiles > 2) load_k(2, 2);
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+  }
+  __syncthreads();
+
+  f32x16 o[HD / 32];
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
+  float m = -1e30f, l = 0.f;
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+  f32x16 S[2];
+  bf16x8 pf[4];
+  pp_qk<HD>(S, smem, qf, kro);
+  pp_softmax<HD>(S, pf, o, m, l, sc, ntiles == 1 ? last_valid : KV, lg);
+  if (!grp_a) __syncthreads();             // group B runs one phase behind
+
+  constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // MFMAs = fragment reads per matrix phase
+  // One tile step with compile-time buffer slot P = t % NB.
+#define WDC_PP4_STEP(P)                                                                          \
+  {                                                                                              \
+    const int t = t0 + (P);                                                                      \
+    int issued = 0;                                                                              \
+    if (grp_a) {                                                                                 \
+      if (t + 3 < ntiles) {                                                                      \
+        load_k(((P) + 3) % NB, t + 3);                                                           \
+        issued += TL::K_STRIPES;                                                                 \
+      }                                                                                          \
+      if (t + 2 < ntiles) {                                                                      \
+        load_v(((P) + 2) % NB, t + 2);                                                           \
+        issued += TL::V_STRIPES;                                                                 \
+      }                                                                                          \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro);                                                 \
+    pp_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro);                                    \
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);                                           \
+    _Pragma("unroll") for (int i_ = 0; i_ < NMF - 4; ++i_) {                                     \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                         \
+    }                                                                                            \
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
+    if (t + 1 < ntiles) pp_softmax<HD>(S, pf, o, m, l, sc, t + 2 < ntiles ? KV : last_valid, lg); \
+    if (grp_a) pp4_wait<HD>(issued);                                                             \
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
+  }
+  for (int t0 = 0; t0 < ntiles; t0 += NB) {
+    WDC_PP4_STEP(0)
+    if (t0 + 1 >= ntiles) break;
+    WDC_PP4_STEP(1)
+    if (t0 + 2 >= ntiles) break;
+    WDC_PP4_STEP(2)
+    if (t0 + 3 >= ntiles) break;
+    WDC_PP4_STEP(3)
+  }
+#undef WDC_PP4_STEP
+  if (grp_a) __syncthreads();              // match group B's extra barrier
+
+  const float lt = l + __shfl_xor(l, 32, 64);
+  const float inv = 1.f / lt;
+  const int64_t q = qbase + lr;
+  if (q < a.n) {
+    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = 32 * i + 8 * g4 + 4 * lg;
+        uint32_t w0 = (uint32_t)f2bf(o[i][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 1] * inv) << 16);
+        uint32_t w1 = (uint32_t)f2bf(o[i][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 3] * inv) << 16);
+        *(uint2 *)(O + d0) = make_uint2(w0, w1);
+      }
+  }
+}
+
+template <int HD>
+hipError_t launch_bf16_pp4(const AttnArgs &a, hipStream_t s) {
+  constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
+  static bool init = false;
+  if (!init) {
+    hipFuncSetAttribute((const void *)k_attn_bf16_pp4<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    init = true;
+  }
+  dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
+  hipLaunchKernelGGL((k_attn_bf16_pp4<HD>), grid, dim3(512), LDS, s, a);
+  return hipGetLastError();
+}
+
 template <int HD>
 hipError_t launch_bf16_pp(const AttnArgs &a, hipStream_t s) {
   constexpr int LDS = (3 + 2) * KV * HD * 2;   // three K tiles, two V^T tiles
@@ -773,9 +946,11 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    // Default: the 8-wave ping-pong kernel (fastest measured at every workload
-    // shape, hd 64 and 128). WDC_ATTN_VARIANT selects the earlier forms:
-    // 0 plain, 1 pipelined one block per CU, 2 pipelined two blocks per CU.
+    // Default: the 8-wave ping-pong kernel, with four-deep tile buffers for
+    // hd 128 (3.9% faster at 67,576 tokens) and the 3 K / 2 V buffer form for
+    // hd 64 (equal within noise at 17,776 tokens, smaller LDS). WDC_ATTN_VARIANT
+    // selects other forms: 0 plain, 1 pipelined one block per CU, 2 pipelined
+    // two blocks per CU, 3 ping-pong 3 K / 2 V, 5 four-deep also for hd 64.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 4;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
@@ -784,11 +959,13 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
       if (variant == 0) return launch_bf16<128, 1>(b, s);
       if (variant == 1) return launch_bf16_pipe<128, 1, 1>(b, s);
       if (variant == 2) return launch_bf16_pipe<128, 1, 2>(b, s);
-      return launch_bf16_pp<128>(b, s);
+      if (variant == 3) return launch_bf16_pp<128>(b, s);
+      return launch_bf16_pp4<128>(b, s);
     }
     if (a.hd == 64) {
       if (variant == 0) return launch_bf16<64, 2>(b, s);
       if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(b, s);
+      if (variant == 5) return launch_bf16_pp4<64>(b, s);
       return launch_bf16_pp<64>(b, s);
     }
     return hipErrorInvalidValue;
