@@ -95,6 +95,7 @@ typedef struct {
   int32_t patch_t, patch_h, patch_w;
   int32_t rope_t, rope_h, rope_w;
   int32_t qk_norm;    /* 1: per-head RMSNorm on q and k */
+  int32_t max_batch;  /* most samples one batched forward takes (0 or 1: one); sizes the workspace */
 } wdc_model_desc;
 
 /* Constants of the method. The paper fixes the anchor-age limit (six) and the
@@ -167,7 +168,7 @@ size_t wdc_workspace_bytes(const wdc_ctx *ctx);
 wdc_status wdc_bind_workspace(wdc_ctx *ctx, void *d_ws, size_t bytes);
 
 /* Rollout state: bank B_t (M exact output latents), anchor, history summary,
- * risk R, eta_d and counters (Sec. 4.2-4.3). Its device memory
+ * risk R, eta_d and counters (Sec. 4.2-4.3), plus the latents a rollout runs on. Its device memory
  * (wdc_state_bytes) is caller-allocated; the state object itself is freed by
  * wdc_state_destroy. h_cam: host float camera vector of cam_dim values for the
  * lifted state's camera descriptor, or NULL (descriptor zero). */
@@ -197,6 +198,17 @@ wdc_status wdc_dit_block_forward(wdc_ctx *ctx, int32_t block, float *d_x, const 
  * the model dtype (text [text_tokens, text_dim]), NULL when absent. */
 wdc_status wdc_dit_forward(wdc_ctx *ctx, const float *d_z, double t, const void *d_cond, const void *d_text,
                            const void *d_cam, float *d_v);
+
+/* Batched F_theta (Sec. 4.4 run for several rollouts at once): v_b =
+ * F_theta(z_b, t, c_b) for b < B <= max_batch, all at the same t. Host arrays
+ * of B device pointers; d_cond/d_text/d_cam may be NULL (no such input) or hold
+ * one pointer per sample. The samples' tokens go through every GEMM as one
+ * batch and through attention as one launch of B x heads; each sample keeps its
+ * own conditioning, modulation and joint attention. Same result per sample as
+ * wdc_dit_forward up to float32 summation order. */
+wdc_status wdc_dit_forward_batch(wdc_ctx *ctx, int32_t B, const float *const *d_z, double t,
+                                 const void *const *d_cond, const void *const *d_text, const void *const *d_cam,
+                                 float *const *d_v);
 
 /* ---------------------------------------------------------------- scheduler Psi_t */
 
@@ -236,6 +248,20 @@ wdc_status wdc_risk_update(wdc_ctx *ctx, wdc_state *st, int32_t phase, int32_t k
 wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const void *d_cond, const void *d_text,
                        const void *d_cam, int32_t mode, const uint8_t *h_forced, const float *d_replay_v,
                        uint8_t *h_schedule, wdc_step_log *h_log);
+
+/* B rollouts at once, each with its own state, latent, conditioning and
+ * schedule (B <= max_batch). Every step runs each sample's candidate and
+ * decision; the samples that take an exact step are evaluated by one batched
+ * F_theta call (or their recorded velocities), the others commit their
+ * candidates. Arrays: states[B]; d_z[B] (in: z_T, out: z_0); d_cond/d_text/d_cam
+ * NULL or [B] pointers; h_forced [B][S] (FORCED only); d_replay_v NULL or [B]
+ * pointers to [S, C, F, H, W] velocities; h_schedule [B][S]; h_log [B][S] or
+ * NULL. Per sample the schedule, log and latent equal those of wdc_rollout on
+ * that sample alone (latents up to float32 summation order). */
+wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, float *const *d_z, int32_t S,
+                             const void *const *d_cond, const void *const *d_text, const void *const *d_cam,
+                             int32_t mode, const uint8_t *h_forced, const float *const *d_replay_v,
+                             uint8_t *h_schedule, wdc_step_log *h_log);
 
 /* ---------------------------------------------------------------- kernels exposed for tests and benchmarks */
 

@@ -32,10 +32,10 @@ class ModelDesc(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "dtype", "hidden", "heads", "head_dim", "mlp_ratio", "n_seq", "n_dual", "n_single", "cond_dim", "cam_dim",
         "text_tokens", "text_dim", "lat_c", "lat_f", "lat_h", "lat_w", "patch_t", "patch_h", "patch_w",
-        "rope_t", "rope_h", "rope_w", "qk_norm")]
+        "rope_t", "rope_h", "rope_w", "qk_norm", "max_batch")]
 
 
-def desc_from_config(cfg) -> ModelDesc:
+def desc_from_config(cfg, max_batch: int = 1) -> ModelDesc:
     """Model descriptor from any object with the workload fields (name, dtype, hidden, ...)."""
     d = ModelDesc()
     d.dtype = WDC_BF16 if cfg.dtype == "bf16" else WDC_F32
@@ -46,6 +46,7 @@ def desc_from_config(cfg) -> ModelDesc:
     d.patch_t, d.patch_h, d.patch_w = cfg.patch
     d.rope_t, d.rope_h, d.rope_w = cfg.rope
     d.qk_norm = int(cfg.qk_norm)
+    d.max_batch = max_batch
     return d
 
 
@@ -107,11 +108,14 @@ def load() -> C.CDLL:
         "wdc_cond_embed": (i32, [vp, dbl, vp, vp, vp]),
         "wdc_dit_block_forward": (i32, [vp, i32, vp, vp]),
         "wdc_dit_forward": (i32, [vp, vp, dbl, vp, vp, vp, vp]),
+        "wdc_dit_forward_batch": (i32, [vp, i32, vp, dbl, vp, vp, vp, vp]),
         "wdc_scheduler_step": (i32, [vp, vp, vp, dbl, dbl, vp, i64]),
         "wdc_surrogate_step": (i32, [vp, vp, vp, i32, i32, vp, C.POINTER(StepLog)]),
         "wdc_risk_update": (i32, [vp, vp, i32, i32, i32, vp, vp, C.POINTER(StepLog)]),
         "wdc_rollout": (i32, [vp, vp, vp, i32, vp, vp, vp, i32, C.POINTER(C.c_uint8), vp, C.POINTER(C.c_uint8),
                               C.POINTER(StepLog)]),
+        "wdc_rollout_batch": (i32, [vp, vp, i32, vp, i32, vp, vp, vp, i32, C.POINTER(C.c_uint8), vp,
+                                    C.POINTER(C.c_uint8), C.POINTER(StepLog)]),
         "wdc_attn_pad": (i64, [i64]),
         "wdc_attention": (i32, [vp, vp, vp, vp, i64, vp, i64]),
         "wdc_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, i64, i64]),
@@ -131,8 +135,8 @@ def exported_symbols() -> List[str]:
         "wdc_params_default", "wdc_create", "wdc_destroy", "wdc_last_error", "wdc_weights_bytes", "wdc_weight_count",
         "wdc_weight_info", "wdc_bind_weights", "wdc_init_weights_random", "wdc_workspace_bytes", "wdc_bind_workspace",
         "wdc_state_bytes", "wdc_state_create", "wdc_state_reset", "wdc_state_destroy", "wdc_state_bank_slot",
-        "wdc_cond_embed", "wdc_dit_block_forward", "wdc_dit_forward", "wdc_scheduler_step", "wdc_surrogate_step",
-        "wdc_risk_update", "wdc_rollout", "wdc_attn_pad", "wdc_attention", "wdc_linear", "wdc_set_timing",
+        "wdc_cond_embed", "wdc_dit_block_forward", "wdc_dit_forward", "wdc_dit_forward_batch", "wdc_scheduler_step",
+        "wdc_surrogate_step", "wdc_risk_update", "wdc_rollout", "wdc_rollout_batch", "wdc_attn_pad", "wdc_attention", "wdc_linear", "wdc_set_timing",
         "wdc_timing"]
 
 
@@ -154,6 +158,13 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _ptrs(ts):
+    """Host array of device pointers of a list of tensors (None entries -> NULL), or None."""
+    if ts is None:
+        return None
+    return (C.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
+
+
 def _torch():
     import torch
     return torch
@@ -164,13 +175,14 @@ class Context:
     rollout state comes from torch allocations."""
 
     def __init__(self, cfg, params: Optional[Params] = None, device: str = "cuda:0", stream=None,
-                 allocate_weights: bool = True):
+                 allocate_weights: bool = True, max_batch: int = 1):
         torch = _torch()
         self.lib = load()
         self.cfg = cfg
         self.device = torch.device(device)
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        self.desc = desc_from_config(cfg)
+        self.max_batch = max_batch
+        self.desc = desc_from_config(cfg, max_batch)
         self.params = params if params is not None else default_params()
         h = C.c_void_p()
         self._check(self.lib.wdc_create(C.byref(self.desc), C.byref(self.params), C.c_void_p(self.stream.cuda_stream),
@@ -269,6 +281,15 @@ class Context:
         self._check(self.lib.wdc_dit_forward(self.h, _ptr(z), t, _ptr(cond), _ptr(text), _ptr(cam), _ptr(out)))
         return out
 
+    def forward_batch(self, zs, t: float, conds=None, texts=None, cams=None, outs=None):
+        """F_theta of len(zs) samples at one t in one batched pass; lists of tensors."""
+        torch = _torch()
+        b = len(zs)
+        outs = outs if outs is not None else [torch.empty_like(z) for z in zs]
+        self._check(self.lib.wdc_dit_forward_batch(self.h, b, _ptrs(zs), t, _ptrs(conds), _ptrs(texts), _ptrs(cams),
+                                                   _ptrs(outs)))
+        return outs
+
     def scheduler_step(self, z, v, t_cur: float, t_next: float, out=None):
         torch = _torch()
         out = out if out is not None else torch.empty_like(z)
@@ -309,6 +330,22 @@ class Context:
         self._check(self.lib.wdc_rollout(self.h, state.h, _ptr(z), steps, _ptr(cond), _ptr(text), _ptr(cam), mode,
                                          fz, _ptr(replay_v), sched, logs))
         return list(sched), [l.as_dict() for l in logs]
+
+    def rollout_batch(self, states: Sequence["State"], zs, steps: int, conds=None, texts=None, cams=None,
+                      mode: int = MODE_RISK, forced: Optional[Sequence[Sequence[int]]] = None, replay_vs=None):
+        """len(zs) rollouts at once (each latent updated in place); per-sample
+        schedules [B][S] and logs [B][S]."""
+        b = len(zs)
+        sched = (C.c_uint8 * (b * steps))()
+        logs = (StepLog * (b * steps))()
+        fz = None
+        if forced is not None:
+            fz = (C.c_uint8 * (b * steps))(*[int(x) for row in forced for x in row])
+        st = (C.c_void_p * b)(*[s.h.value for s in states])
+        self._check(self.lib.wdc_rollout_batch(self.h, st, b, _ptrs(zs), steps, _ptrs(conds), _ptrs(texts),
+                                               _ptrs(cams), mode, fz, _ptrs(replay_vs), sched, logs))
+        return ([list(sched[i * steps:(i + 1) * steps]) for i in range(b)],
+                [[logs[i * steps + k].as_dict() for k in range(steps)] for i in range(b)])
 
     def surrogate_step(self, state: "State", z, k: int, steps: int, zhat) -> dict:
         log = StepLog()

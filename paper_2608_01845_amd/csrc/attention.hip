@@ -26,6 +26,16 @@ namespace {
 
 // ---------------------------------------------------------------- float32 reference-style kernel
 // 16 queries per block, 16 threads per query, each thread owns hd/16 dims.
+// Output offset of query q of head h: with several samples in one launch, head
+// h is head h % hpb of sample h / hpb, whose rows start at sample * n.
+__device__ __forceinline__ int64_t out_off(const AttnArgs &a, int h, int64_t q, int hd) {
+  if (a.hpb > 0) {
+    const int smp = h / a.hpb;
+    return ((int64_t)smp * a.n + q) * a.ldo + (int64_t)(h - smp * a.hpb) * hd;
+  }
+  return q * a.ldo + (int64_t)h * hd;
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a) {
   constexpr int PER = HD / 16;
@@ -72,7 +82,7 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a) {
     __syncthreads();
   }
   if (q < a.n) {
-    float *O = (float *)a.o + q * a.ldo + (int64_t)h * HD + part * PER;
+    float *O = (float *)a.o + out_off(a, h, q, HD) + part * PER;
 #pragma unroll
     for (int i = 0; i < PER; ++i) O[i] = o[i] / l;
   }
@@ -312,7 +322,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     const float inv = 1.f / lt;
     const int64_t q = qbase + 32 * qt + lr;
     if (q >= a.n) continue;
-    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
 #pragma unroll
     for (int i = 0; i < C::NH; ++i)
 #pragma unroll
@@ -512,7 +522,7 @@ __global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
     const float inv = 1.f / lt;
     const int64_t q = qbase + 32 * qt + lr;
     if (q >= a.n) continue;
-    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
 #pragma unroll
     for (int i = 0; i < C::NH; ++i)
 #pragma unroll
@@ -715,7 +725,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp(AttnArgs a) {
   const float inv = 1.f / lt;
   const int64_t q = qbase + lr;
   if (q < a.n) {
-    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
 #pragma unroll
     for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
@@ -875,7 +885,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
   const float inv = 1.f / lt;
   const int64_t q = qbase + lr;
   if (q < a.n) {
-    bf16_t *O = (bf16_t *)a.o + q * a.ldo + (int64_t)h * HD;
+    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
 #pragma unroll
     for (int i = 0; i < HD / 32; ++i)
 #pragma unroll

@@ -97,6 +97,10 @@ struct GemmArgs {
   int64_t lda, ldc;
   int64_t m, n, k;
   int epi;
+  // batch of independent products on grid z: entry z reads a + z*a_bs and
+  // writes c + z*c_bs (elements) with gate + z*gate_bs; batch 0 or 1 = one
+  int batch;
+  int64_t a_bs, c_bs, gate_bs;
 };
 
 // dtype: 0 float32, 1 bfloat16
@@ -109,13 +113,24 @@ struct AttnArgs {
   int64_t n, n_pad, ldo;
   int heads, hd;
   int xcd_order;          // 1: blocks of one head run together on one XCD (heads % 8 == 0)
+  // heads per sample when several samples share one launch: head index h is
+  // (sample h / hpb, head h % hpb), whose rows start at sample * n in o;
+  // 0 = one sample
+  int hpb;
 };
 int64_t attn_pad(int64_t n);
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
 
 // ------------------------------------------------------------------ elementwise and small kernels
-// h[r, :] = LN(x[r, :]) * (1 + scale) + shift for rows [0, rows); x float32, h model dtype.
-hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, int64_t rows, int d,
+// h[r, :] = LN(x[r, :]) * (1 + scale) + shift; x float32, h model dtype.
+// Rows come in groups of rps (one sample each): logical row i is row
+// (i / rps) * sstride + i % rps of x and h, and uses shift/scale + (i / rps) * mstride.
+struct LnRows {
+  int64_t rows;             // logical rows in total
+  int64_t rps, sstride;     // rows per sample, row distance between samples
+  int64_t mstride;          // floats between samples' shift/scale vectors
+};
+hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, const LnRows &r, int d,
                          const float *shift, const float *scale, hipStream_t s);
 
 // Split q/k/v from a fused projection output into attention layout; per-head

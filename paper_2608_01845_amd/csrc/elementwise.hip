@@ -12,10 +12,14 @@ namespace {
 // passes (mean, then variance of the centred values).
 template <typename T, int MAXV>
 __global__ __launch_bounds__(256) void k_ln_mod(const float *__restrict__ x, int64_t ldx, T *__restrict__ h,
-                                               int64_t ldh, int d, const float *__restrict__ shift,
+                                               int64_t ldh, LnRows lr, int d, const float *__restrict__ shift,
                                                const float *__restrict__ scale) {
   __shared__ float red[8];
-  const int64_t r = blockIdx.x;
+  const int64_t i = blockIdx.x;
+  const int64_t smp = i / lr.rps;
+  const int64_t r = smp * lr.sstride + i % lr.rps;
+  shift += smp * lr.mstride;
+  scale += smp * lr.mstride;
   const float *xr = x + r * ldx;
   float v[MAXV];
   float s = 0.f;
@@ -285,21 +289,21 @@ __global__ void k_copy_rows(const float *src, int64_t lds, float *dst, int64_t l
 inline unsigned nblk(int64_t n, int t) { return (unsigned)((n + t - 1) / t); }
 }  // namespace
 
-hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, int64_t rows, int d,
+hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, const LnRows &r, int d,
                          const float *shift, const float *scale, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  if (d > 16 * 256) return hipErrorInvalidValue;
-  dim3 g((unsigned)rows), b(256);
+  if (r.rows <= 0) return hipSuccess;
+  if (d > 16 * 256 || r.rps <= 0 || r.sstride < r.rps) return hipErrorInvalidValue;
+  dim3 g((unsigned)r.rows), b(256);
   if (dtype == 1) {
     if (d <= 4 * 256)
-      hipLaunchKernelGGL((k_ln_mod<bf16_t, 4>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, d, shift, scale);
+      hipLaunchKernelGGL((k_ln_mod<bf16_t, 4>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, r, d, shift, scale);
     else
-      hipLaunchKernelGGL((k_ln_mod<bf16_t, 16>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, d, shift, scale);
+      hipLaunchKernelGGL((k_ln_mod<bf16_t, 16>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, r, d, shift, scale);
   } else {
     if (d <= 4 * 256)
-      hipLaunchKernelGGL((k_ln_mod<float, 4>), g, b, 0, s, x, ldx, (float *)h, ldh, d, shift, scale);
+      hipLaunchKernelGGL((k_ln_mod<float, 4>), g, b, 0, s, x, ldx, (float *)h, ldh, r, d, shift, scale);
     else
-      hipLaunchKernelGGL((k_ln_mod<float, 16>), g, b, 0, s, x, ldx, (float *)h, ldh, d, shift, scale);
+      hipLaunchKernelGGL((k_ln_mod<float, 16>), g, b, 0, s, x, ldx, (float *)h, ldh, r, d, shift, scale);
   }
   return hipGetLastError();
 }

@@ -30,8 +30,23 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, int epi, int64_t row
 }
 
 // ---------------------------------------------------------------- generic tiled kernel
+// Batch entry blockIdx.z of a batched product: shifted operand and output pointers.
 template <typename T>
-__global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g) {
+__device__ __forceinline__ GemmArgs batch_entry(const GemmArgs &g0) {
+  GemmArgs g = g0;
+  const int64_t z = blockIdx.z;
+  if (z) {
+    const bool c16 = (g0.epi == EPI_STORE || g0.epi == EPI_GELU) && sizeof(T) == 2;
+    g.a = (const T *)g0.a + z * g0.a_bs;
+    g.c = c16 ? (void *)((T *)g0.c + z * g0.c_bs) : (void *)((float *)g0.c + z * g0.c_bs);
+    if (g0.gate) g.gate = g0.gate + z * g0.gate_bs;
+  }
+  return g;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g0) {
+  const GemmArgs g = batch_entry<T>(g0);
   __shared__ float As[16][64 + 4];
   __shared__ float Bs[16][64 + 4];
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
@@ -109,8 +124,9 @@ __device__ __forceinline__ float epi_act(float v) {
 }
 
 template <int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g) {
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   using C = Cfg<BM, BN, WM, WN>;
+  const GemmArgs g = batch_entry<bf16_t>(g0);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char *sA = smem;                      // [2][BM][128 B]
   char *sB = smem + 2 * BM * BK * 2;    // [2][BN][128 B]
@@ -239,7 +255,7 @@ template <int BM, int BN, int WM, int WN>
 hipError_t launch_mfma(const GemmArgs &g, hipStream_t s) {
   using C = Cfg<BM, BN, WM, WN>;
   const int m_tiles = (int)((g.m + BM - 1) / BM), n_tiles = (int)(g.n / BN);
-  dim3 grid(m_tiles * n_tiles), block(C::NT);
+  dim3 grid(m_tiles * n_tiles, 1, g.batch > 1 ? g.batch : 1), block(C::NT);
   switch (g.epi) {
     case EPI_STORE: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GELU: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>), grid, block, C::LDS_BYTES, s, g); break;
@@ -275,7 +291,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
       return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s) : launch_mfma<256, 256, 2, 4>(g, s);
     if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
   }
-  dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64)), block(256);
+  dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64), g.batch > 1 ? g.batch : 1), block(256);
   if (dtype == 1)
     hipLaunchKernelGGL(k_gemm_simple<bf16_t>, grid, block, 0, s, g);
   else

@@ -40,6 +40,8 @@ struct wdc_ctx {
   int esz = 4;
   // derived shapes
   int64_t nv = 0, nt = 0, n = 0, n_pad = 0, E = 0, T = 0;
+  int mb = 1;  // most samples of one batched forward (workspace sizing)
+  int nb = 1;  // samples of the forward in progress
   int P = 0, D = 0, H = 0, hd = 0, F = 0;
   // weights
   std::vector<TensorInfo> tensors;
@@ -53,7 +55,7 @@ struct wdc_ctx {
   void *h = nullptr, *qkv = nullptr, *cat = nullptr, *q = nullptr, *k = nullptr, *v = nullptr, *patches = nullptr;
   float *tok = nullptr;
   float2 *rope = nullptr;
-  float *r_v = nullptr, *r_zhat = nullptr, *r_zcur = nullptr, *r_znext = nullptr;
+  float *r_v = nullptr;  // [mb, E] velocities of a batched forward inside a rollout
   // timing
   bool timing = false;
   std::vector<TimedEvent> events;
@@ -86,6 +88,7 @@ struct wdc_state {
   double cam[GCAM];
   double R = 0, eta = 1;
   int n_s = 0;
+  float *rz[3] = {nullptr, nullptr, nullptr};  // current latent, candidate, next exact latent of a rollout
   float *partials = nullptr;
   double *d_red = nullptr;
   double *h_red = nullptr;  // pinned host
@@ -209,36 +212,36 @@ struct Carve {
 };
 
 struct WsLayout {
-  size_t x, h, qkv, cat, q, k, v, mod, cemb, tfeat, tmp, cvec, patches, tok, rope, rv, rzhat, rzcur, rznext, total;
+  size_t x, h, qkv, cat, q, k, v, mod, cemb, tfeat, tmp, cvec, patches, tok, rope, rv, total;
 };
+
+// per-sample stride of the modulation vectors (dual blocks use 12 D)
+int64_t mod_stride(const wdc_ctx *c) { return 12 * (int64_t)c->D; }
 
 WsLayout ws_layout(const wdc_ctx *c) {
   WsLayout L;
   Carve cv;
-  const size_t e = c->esz, D = c->D, N = c->n;
+  const size_t e = c->esz, D = c->D, B = c->mb, N = c->n * B;
   const size_t f = (size_t)c->d.mlp_ratio * D;
   const size_t E = c->E;
   L.x = cv.take(N * D * 4);
   L.h = cv.take(N * D * e);
   L.qkv = cv.take(N * 3 * D * e);
   L.cat = cv.take(N * (D + f) * e);
-  size_t qk = (size_t)c->H * c->n_pad * c->hd * e;
+  size_t qk = B * c->H * c->n_pad * c->hd * e;
   L.q = cv.take(qk);
   L.k = cv.take(qk);
   L.v = cv.take(qk);
-  L.mod = cv.take(12 * D * 4);
-  L.cemb = cv.take(D * 4);
+  L.mod = cv.take(B * mod_stride(c) * 4);
+  L.cemb = cv.take(B * D * 4);
   L.tfeat = cv.take(256 * 4);
   L.tmp = cv.take(D * 4);
   size_t cdim = std::max({(size_t)c->d.cond_dim, (size_t)c->d.cam_dim, (size_t)1});
   L.cvec = cv.take(cdim * 4);
-  L.patches = cv.take((size_t)c->nv * c->P * e);
-  L.tok = cv.take((size_t)c->nv * c->P * 4);
+  L.patches = cv.take(B * c->nv * c->P * e);
+  L.tok = cv.take(B * c->nv * c->P * 4);
   L.rope = cv.take((size_t)c->nv * (c->hd / 2) * 8);
-  L.rv = cv.take(E * 4);
-  L.rzhat = cv.take(E * 4);
-  L.rzcur = cv.take(E * 4);
-  L.rznext = cv.take(E * 4);
+  L.rv = cv.take(B * E * 4);
   L.total = cv.off;
   return L;
 }
@@ -261,14 +264,23 @@ hipError_t timed(wdc_ctx *c, int cls, double work, F &&fn) {
 }
 
 // ---------------------------------------------------------------- kernel wrappers
+char *elem(wdc_ctx *c, void *base, int64_t off) { return (char *)base + off * c->esz; }
+const char *elem(wdc_ctx *c, const void *base, int64_t off) { return (const char *)base + off * c->esz; }
+
+// a batch of n products sharing weights; strides in elements (gate in floats)
+struct Batch {
+  int n = 1;
+  int64_t a_bs = 0, c_bs = 0, gate_bs = 0;
+};
+
 wdc_status gemm(wdc_ctx *c, const void *a, int64_t lda, const void *w, const void *b, void *out, int64_t ldc,
-                int64_t m, int64_t n, int64_t k, int epi, const float *gate = nullptr) {
-  if (m <= 0) return WDC_OK;
+                int64_t m, int64_t n, int64_t k, int epi, const float *gate = nullptr, Batch bt = Batch()) {
+  if (m <= 0 || bt.n <= 0) return WDC_OK;
   if (!w) {
     set_err(c, "weights not bound");
     return WDC_E_WORKSPACE;
   }
-  GemmArgs g;
+  GemmArgs g{};
   g.a = a;
   g.w = w;
   g.bias = b;
@@ -280,7 +292,11 @@ wdc_status gemm(wdc_ctx *c, const void *a, int64_t lda, const void *w, const voi
   g.n = n;
   g.k = k;
   g.epi = epi;
-  HIPCHK(c, timed(c, WDC_T_GEMM, 2.0 * m * n * k, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
+  g.batch = bt.n;
+  g.a_bs = bt.a_bs;
+  g.c_bs = bt.c_bs;
+  g.gate_bs = bt.gate_bs;
+  HIPCHK(c, timed(c, WDC_T_GEMM, 2.0 * m * n * k * bt.n, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
   return WDC_OK;
 }
 
@@ -295,8 +311,17 @@ wdc_status gemv(wdc_ctx *c, const std::string &name, const float *x, float *y, i
   return WDC_OK;
 }
 
+// the modulation GEMV of every sample: y_b = W SiLU(cemb_b) + b, at mod + b * mod_stride + off
+wdc_status mod_gemv(wdc_ctx *c, const std::string &name, int64_t off) {
+  for (int b = 0; b < c->nb; ++b)
+    CHK(gemv(c, name, c->cemb + (int64_t)b * c->D, c->mod + b * mod_stride(c) + off, 1, 0));
+  return WDC_OK;
+}
+
+// joint attention of every sample: q/k/v hold nb x H heads, O rows follow the samples
 wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
-  HIPCHK(c, launch_qkv_pad(c->d.dtype, c->q, c->k, c->v, c->H, c->hd, c->n, c->n_pad, c->stream));
+  const int hb = c->H * c->nb;
+  HIPCHK(c, launch_qkv_pad(c->d.dtype, c->q, c->k, c->v, hb, c->hd, c->n, c->n_pad, c->stream));
   AttnArgs a{};
   a.q = c->q;
   a.k = c->k;
@@ -305,67 +330,83 @@ wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
   a.n = c->n;
   a.n_pad = c->n_pad;
   a.ldo = ldo;
-  a.heads = c->H;
+  a.heads = hb;
   a.hd = c->hd;
-  const double aw = 4.0 * (double)c->n * (double)c->n * c->hd * c->H;
+  a.hpb = c->H;
+  const double aw = 4.0 * (double)c->n * (double)c->n * c->hd * hb;
   HIPCHK(c, timed(c, WDC_T_ATTENTION, aw, [&] { return launch_attention(c->d.dtype, a, c->stream); }));
   return WDC_OK;
 }
 
+// q/k/v of every sample from the fused projection rows [row0, row0 + rows) of
+// each sample (row stride ld) into the attention layouts of its heads
 wdc_status qkv_prep(wdc_ctx *c, const void *src, int64_t ld, int64_t row0, int64_t rows) {
-  QKVPrepArgs a;
-  a.src = src;
-  a.ld = ld;
-  a.row0 = row0;
-  a.rows = rows;
-  a.n_video = c->nv;
-  a.n_pad = c->n_pad;
-  a.q = c->q;
-  a.k = c->k;
-  a.v = c->v;
-  a.heads = c->H;
-  a.hd = c->hd;
-  a.d = c->D;
-  a.qk_norm = c->d.qk_norm;
-  a.rope = (c->d.rope_t + c->d.rope_h + c->d.rope_w) ? c->rope : nullptr;
-  HIPCHK(c, launch_qkv_prep(c->d.dtype, a, c->stream));
+  const int64_t hs = (int64_t)c->H * c->n_pad * c->hd;  // elements per sample of q/k/v
+  for (int b = 0; b < c->nb; ++b) {
+    QKVPrepArgs a;
+    a.src = elem(c, src, (int64_t)b * c->n * ld);
+    a.ld = ld;
+    a.row0 = row0;
+    a.rows = rows;
+    a.n_video = c->nv;
+    a.n_pad = c->n_pad;
+    a.q = elem(c, c->q, b * hs);
+    a.k = elem(c, c->k, b * hs);
+    a.v = elem(c, c->v, b * hs);
+    a.heads = c->H;
+    a.hd = c->hd;
+    a.d = c->D;
+    a.qk_norm = c->d.qk_norm;
+    a.rope = (c->d.rope_t + c->d.rope_h + c->d.rope_w) ? c->rope : nullptr;
+    HIPCHK(c, launch_qkv_prep(c->d.dtype, a, c->stream));
+  }
   return WDC_OK;
 }
 
-char *elem(wdc_ctx *c, void *base, int64_t off) { return (char *)base + off * c->esz; }
-
+// LayerNorm + modulation of rows [row0, row0 + rows) of every sample, with the
+// shift/scale vectors of sample 0 given (the others follow at mod_stride)
 wdc_status ln_mod(wdc_ctx *c, int64_t row0, int64_t rows, const float *shift, const float *scale) {
-  HIPCHK(c, timed(c, WDC_T_NORM, (double)rows * c->D * (4 + c->esz), [&] {
-    return launch_ln_mod(c->d.dtype, c->x + row0 * c->D, c->D, elem(c, c->h, row0 * c->D), c->D, rows, c->D, shift,
+  LnRows r;
+  r.rows = rows * c->nb;
+  r.rps = rows;
+  r.sstride = c->n;
+  r.mstride = mod_stride(c);
+  HIPCHK(c, timed(c, WDC_T_NORM, (double)r.rows * c->D * (4 + c->esz), [&] {
+    return launch_ln_mod(c->d.dtype, c->x + row0 * c->D, c->D, elem(c, c->h, row0 * c->D), c->D, r, c->D, shift,
                          scale, c->stream);
   }));
   return WDC_OK;
 }
 
 // ---------------------------------------------------------------- blocks
+// Every block works on all nb samples of the residual stream x [nb, N, D]:
+// products that share weights and need no per-sample vector run as one GEMM
+// over all rows; gated residual products run as a batch (one gate per sample).
 wdc_status seq_block(wdc_ctx *c, int i) {
-  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F;
+  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F, NB = c->nb, MS = mod_stride(c);
   const std::string pre = "seq." + std::to_string(i);
   float *m = c->mod;
-  CHK(gemv(c, pre + ".ada", c->cemb, m, 1, 0));
+  const Batch gr{(int)NB, N * LC, N * D, MS};
+  CHK(mod_gemv(c, pre + ".ada", 0));
   CHK(ln_mod(c, 0, N, m, m + D));
-  CHK(gemm(c, c->h, D, W(c, pre + ".qkv.w"), W(c, pre + ".qkv.b"), c->qkv, 3 * D, N, 3 * D, D, EPI_STORE));
+  CHK(gemm(c, c->h, D, W(c, pre + ".qkv.w"), W(c, pre + ".qkv.b"), c->qkv, 3 * D, NB * N, 3 * D, D, EPI_STORE));
   CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
   CHK(attention(c, c->cat, LC));
-  CHK(gemm(c, c->cat, LC, W(c, pre + ".out.w"), W(c, pre + ".out.b"), c->x, D, N, D, D, EPI_GATE_RES, m + 2 * D));
+  CHK(gemm(c, c->cat, LC, W(c, pre + ".out.w"), W(c, pre + ".out.b"), c->x, D, N, D, D, EPI_GATE_RES, m + 2 * D, gr));
   CHK(ln_mod(c, 0, N, m + 3 * D, m + 4 * D));
-  CHK(gemm(c, c->h, D, W(c, pre + ".fc1.w"), W(c, pre + ".fc1.b"), elem(c, c->cat, D), LC, N, F, D, EPI_GELU));
+  CHK(gemm(c, c->h, D, W(c, pre + ".fc1.w"), W(c, pre + ".fc1.b"), elem(c, c->cat, D), LC, NB * N, F, D,
+           EPI_GELU));
   CHK(gemm(c, elem(c, c->cat, D), LC, W(c, pre + ".fc2.w"), W(c, pre + ".fc2.b"), c->x, D, N, D, F, EPI_GATE_RES,
-           m + 5 * D));
+           m + 5 * D, gr));
   return WDC_OK;
 }
 
 wdc_status dual_block(wdc_ctx *c, int i) {
-  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F, NV = c->nv, NT = c->nt;
+  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F, NV = c->nv, NT = c->nt, NB = c->nb, MS = mod_stride(c);
   const std::string pre = "dual." + std::to_string(i);
   float *mv = c->mod, *mt = c->mod + 6 * D;
-  CHK(gemv(c, pre + ".vid.ada", c->cemb, mv, 1, 0));
-  CHK(gemv(c, pre + ".txt.ada", c->cemb, mt, 1, 0));
+  CHK(mod_gemv(c, pre + ".vid.ada", 0));
+  CHK(mod_gemv(c, pre + ".txt.ada", 6 * D));
   const struct {
     const char *s;
     int64_t r0, rows;
@@ -375,39 +416,41 @@ wdc_status dual_block(wdc_ctx *c, int i) {
     std::string p = pre + "." + s.s;
     CHK(ln_mod(c, s.r0, s.rows, s.m, s.m + D));
     CHK(gemm(c, elem(c, c->h, s.r0 * D), D, W(c, p + ".qkv.w"), W(c, p + ".qkv.b"), elem(c, c->qkv, s.r0 * 3 * D),
-             3 * D, s.rows, 3 * D, D, EPI_STORE));
+             3 * D, s.rows, 3 * D, D, EPI_STORE, nullptr, Batch{(int)NB, N * D, N * 3 * D, 0}));
   }
   CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
   CHK(attention(c, c->cat, LC));
   for (auto &s : st) {
     std::string p = pre + "." + s.s;
     CHK(gemm(c, elem(c, c->cat, s.r0 * LC), LC, W(c, p + ".out.w"), W(c, p + ".out.b"), c->x + s.r0 * D, D, s.rows,
-             D, D, EPI_GATE_RES, s.m + 2 * D));
+             D, D, EPI_GATE_RES, s.m + 2 * D, Batch{(int)NB, N * LC, N * D, MS}));
     CHK(ln_mod(c, s.r0, s.rows, s.m + 3 * D, s.m + 4 * D));
     CHK(gemm(c, elem(c, c->h, s.r0 * D), D, W(c, p + ".fc1.w"), W(c, p + ".fc1.b"), elem(c, c->cat, s.r0 * LC + D),
-             LC, s.rows, F, D, EPI_GELU));
+             LC, s.rows, F, D, EPI_GELU, nullptr, Batch{(int)NB, N * D, N * LC, 0}));
     CHK(gemm(c, elem(c, c->cat, s.r0 * LC + D), LC, W(c, p + ".fc2.w"), W(c, p + ".fc2.b"), c->x + s.r0 * D, D,
-             s.rows, D, F, EPI_GATE_RES, s.m + 5 * D));
+             s.rows, D, F, EPI_GATE_RES, s.m + 5 * D, Batch{(int)NB, N * LC, N * D, MS}));
   }
   return WDC_OK;
 }
 
 wdc_status single_block(wdc_ctx *c, int i) {
-  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F;
+  const int64_t D = c->D, N = c->n, F = c->F, LC = D + F, NB = c->nb, MS = mod_stride(c);
   const std::string pre = "single." + std::to_string(i);
   float *m = c->mod;
-  CHK(gemv(c, pre + ".ada", c->cemb, m, 1, 0));
+  CHK(mod_gemv(c, pre + ".ada", 0));
   CHK(ln_mod(c, 0, N, m, m + D));
   const char *w1 = (const char *)W(c, pre + ".lin1.w"), *b1 = (const char *)W(c, pre + ".lin1.b");
   if (!w1) {
     set_err(c, "weights not bound");
     return WDC_E_WORKSPACE;
   }
-  CHK(gemm(c, c->h, D, w1, b1, c->qkv, 3 * D, N, 3 * D, D, EPI_STORE));
-  CHK(gemm(c, c->h, D, w1 + 3 * D * D * c->esz, b1 + 3 * D * c->esz, elem(c, c->cat, D), LC, N, F, D, EPI_GELU));
+  CHK(gemm(c, c->h, D, w1, b1, c->qkv, 3 * D, NB * N, 3 * D, D, EPI_STORE));
+  CHK(gemm(c, c->h, D, w1 + 3 * D * D * c->esz, b1 + 3 * D * c->esz, elem(c, c->cat, D), LC, NB * N, F, D,
+           EPI_GELU));
   CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
   CHK(attention(c, c->cat, LC));
-  CHK(gemm(c, c->cat, LC, W(c, pre + ".lin2.w"), W(c, pre + ".lin2.b"), c->x, D, N, D, LC, EPI_GATE_RES, m + 2 * D));
+  CHK(gemm(c, c->cat, LC, W(c, pre + ".lin2.w"), W(c, pre + ".lin2.b"), c->x, D, N, D, LC, EPI_GATE_RES, m + 2 * D,
+           Batch{(int)NB, N * LC, N * D, MS}));
   return WDC_OK;
 }
 
@@ -457,32 +500,53 @@ wdc_status cond_embed(wdc_ctx *c, double t, const void *cond, const void *cam, f
   return WDC_OK;
 }
 
-wdc_status dit_forward(wdc_ctx *c, const float *z, double t, const void *cond, const void *text, const void *cam,
-                       float *vout) {
+// F_theta of nb samples at one time t (inputs per sample; cond/text/cam arrays may be null)
+wdc_status dit_forward_batch(wdc_ctx *c, int nb, const float *const *z, double t, const void *const *cond,
+                             const void *const *text, const void *const *cam, float *const *vout) {
   CHK(need_ws(c));
   CHK(need_w(c));
-  const int64_t D = c->D;
-  CHK(cond_embed(c, t, cond, cam, c->cemb));
+  if (nb < 1 || nb > c->mb) {
+    set_err(c, "batch of %d samples outside 1..%d (max_batch)", nb, c->mb);
+    return WDC_E_ARG;
+  }
+  struct Restore {
+    wdc_ctx *c;
+    ~Restore() { c->nb = 1; }
+  } restore{c};
+  c->nb = nb;
+  const int64_t D = c->D, N = c->n, NV = c->nv, P = c->P;
   const auto &d = c->d;
-  HIPCHK(c, launch_patchify(d.dtype, z, c->patches, d.lat_c, d.lat_f, d.lat_h, d.lat_w, d.patch_t, d.patch_h,
-                            d.patch_w, c->stream));
-  CHK(gemm(c, c->patches, c->P, W(c, "patch_embed.w"), W(c, "patch_embed.b"), c->x, D, c->nv, D, c->P,
-           EPI_STORE_F32));
+  for (int b = 0; b < nb; ++b)
+    CHK(cond_embed(c, t, cond ? cond[b] : nullptr, cam ? cam[b] : nullptr, c->cemb + b * D));
+  for (int b = 0; b < nb; ++b)
+    HIPCHK(c, launch_patchify(d.dtype, z[b], elem(c, c->patches, b * NV * P), d.lat_c, d.lat_f, d.lat_h, d.lat_w,
+                              d.patch_t, d.patch_h, d.patch_w, c->stream));
+  CHK(gemm(c, c->patches, P, W(c, "patch_embed.w"), W(c, "patch_embed.b"), c->x, D, NV, D, P, EPI_STORE_F32, nullptr,
+           Batch{nb, NV * P, N * D, 0}));
   if (d.text_tokens) {
-    if (!text) {
-      set_err(c, "model has text tokens but d_text is NULL");
-      return WDC_E_ARG;
+    for (int b = 0; b < nb; ++b) {
+      if (!text || !text[b]) {
+        set_err(c, "model has text tokens but d_text is NULL");
+        return WDC_E_ARG;
+      }
+      CHK(gemm(c, text[b], d.text_dim, W(c, "text_proj.w"), W(c, "text_proj.b"), c->x + (b * N + NV) * D, D, c->nt,
+               D, d.text_dim, EPI_STORE_F32));
     }
-    CHK(gemm(c, text, d.text_dim, W(c, "text_proj.w"), W(c, "text_proj.b"), c->x + c->nv * D, D, c->nt, D,
-             d.text_dim, EPI_STORE_F32));
   }
   for (int b = 0; b < d.n_seq + d.n_dual + d.n_single; ++b) CHK(block_forward(c, b));
-  CHK(gemv(c, "final.ada", c->cemb, c->mod, 1, 0));
-  CHK(ln_mod(c, 0, c->nv, c->mod, c->mod + D));
-  CHK(gemm(c, c->h, D, W(c, "final.lin.w"), W(c, "final.lin.b"), c->tok, c->P, c->nv, c->P, D, EPI_STORE_F32));
-  HIPCHK(c, launch_unpatchify(c->tok, vout, d.lat_c, d.lat_f, d.lat_h, d.lat_w, d.patch_t, d.patch_h, d.patch_w,
-                              c->stream));
+  CHK(mod_gemv(c, "final.ada", 0));
+  CHK(ln_mod(c, 0, NV, c->mod, c->mod + D));
+  CHK(gemm(c, c->h, D, W(c, "final.lin.w"), W(c, "final.lin.b"), c->tok, P, NV, P, D, EPI_STORE_F32, nullptr,
+           Batch{nb, N * D, NV * P, 0}));
+  for (int b = 0; b < nb; ++b)
+    HIPCHK(c, launch_unpatchify(c->tok + b * NV * P, vout[b], d.lat_c, d.lat_f, d.lat_h, d.lat_w, d.patch_t,
+                                d.patch_h, d.patch_w, c->stream));
   return WDC_OK;
+}
+
+wdc_status dit_forward(wdc_ctx *c, const float *z, double t, const void *cond, const void *text, const void *cam,
+                       float *vout) {
+  return dit_forward_batch(c, 1, &z, t, &cond, &text, &cam, &vout);
 }
 
 // ---------------------------------------------------------------- surrogate / risk (host float64)
@@ -981,6 +1045,12 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
     delete c;
     return WDC_E_ARG;
   }
+  if (d.max_batch < 0 || d.max_batch > 64) {
+    g_create_err = "max_batch out of range (0..64)";
+    delete c;
+    return WDC_E_ARG;
+  }
+  c->mb = d.max_batch > 1 ? d.max_batch : 1;
   c->stream = (hipStream_t)stream;
   c->esz = d.dtype == WDC_BF16 ? 2 : 4;
   c->D = d.hidden;
@@ -1087,9 +1157,6 @@ wdc_status wdc_bind_workspace(wdc_ctx *ctx, void *d_ws, size_t bytes) {
   ctx->tok = (float *)(b + L.tok);
   ctx->rope = (float2 *)(b + L.rope);
   ctx->r_v = (float *)(b + L.rv);
-  ctx->r_zhat = (float *)(b + L.rzhat);
-  ctx->r_zcur = (float *)(b + L.rzcur);
-  ctx->r_znext = (float *)(b + L.rznext);
   const auto &d = ctx->d;
   if (d.rope_t + d.rope_h + d.rope_w > 0 && ctx->nv > 0) {
     // rotation table in float64, rounded once: pair j of axis a turns by pos_a * 1e4^(-2j/d_a)
@@ -1125,7 +1192,7 @@ size_t wdc_state_bytes(const wdc_ctx *ctx) {
   size_t lat = (((size_t)ctx->E * 4 + 255) / 256) * 256;
   size_t part = (((size_t)pl.nblocks() * POST_NV * 4 + 255) / 256) * 256;
   size_t red = (((size_t)pl.nseg() * POST_NV * 8 + 255) / 256) * 256;
-  return lat * n_latents(ctx) + part + red;
+  return lat * (n_latents(ctx) + 3) + part + red;
 }
 
 wdc_status wdc_state_create(wdc_ctx *ctx, void *d_mem, size_t bytes, wdc_state **out) {
@@ -1149,7 +1216,8 @@ wdc_status wdc_state_create(wdc_ctx *ctx, void *d_mem, size_t bytes, wdc_state *
   if (ctx->p.observation == WDC_OBS_LINEAR)
     for (int i = 0; i < ctx->p.bank_capacity; ++i)
       st->bank_in[i] = (float *)(b + lat * (2 + ctx->p.bank_capacity + i));
-  size_t o = lat * n_latents(ctx);
+  for (int i = 0; i < 3; ++i) st->rz[i] = (float *)(b + lat * (n_latents(ctx) + i));
+  size_t o = lat * (n_latents(ctx) + 3);
   st->partials = (float *)(b + o);
   o += (((size_t)st->plan.nblocks() * POST_NV * 4 + 255) / 256) * 256;
   st->d_red = (double *)(b + o);
@@ -1261,11 +1329,25 @@ wdc_status wdc_risk_update(wdc_ctx *ctx, wdc_state *st, int32_t phase, int32_t k
   }
 }
 
-wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const void *d_cond, const void *d_text,
-                       const void *d_cam, int32_t mode, const uint8_t *h_forced, const float *d_replay_v,
-                       uint8_t *h_schedule, wdc_step_log *h_log) {
-  if (!ctx || !st || st->ctx != ctx || !d_z || S < 1 || !h_schedule) return WDC_E_ARG;
+wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, float *const *d_z, int32_t S,
+                             const void *const *d_cond, const void *const *d_text, const void *const *d_cam,
+                             int32_t mode, const uint8_t *h_forced, const float *const *d_replay_v,
+                             uint8_t *h_schedule, wdc_step_log *h_log) {
+  if (!ctx || !states || !d_z || S < 1 || !h_schedule || B < 1) return WDC_E_ARG;
   if (mode < WDC_MODE_RISK || mode > WDC_MODE_PERIODIC || (mode == WDC_MODE_FORCED && !h_forced)) return WDC_E_ARG;
+  if (B > ctx->mb) {
+    set_err(ctx, "batch of %d rollouts exceeds max_batch %d", B, ctx->mb);
+    return WDC_E_ARG;
+  }
+  for (int b = 0; b < B; ++b) {
+    if (!states[b] || states[b]->ctx != ctx || !d_z[b]) return WDC_E_ARG;
+    for (int j = 0; j < b; ++j)
+      if (states[j] == states[b]) {
+        set_err(ctx, "rollouts of one batch need distinct states");
+        return WDC_E_ARG;
+      }
+    if (d_replay_v && !d_replay_v[b]) return WDC_E_ARG;
+  }
   CHK(need_ws(ctx));
   if (!d_replay_v) {
     CHK(need_w(ctx));
@@ -1274,45 +1356,102 @@ wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const
       return WDC_E_STATE;
     }
   }
-  std::vector<float> cam;
-  if (d_cam && ctx->d.cam_dim > 0) {
-    cam.resize(ctx->d.cam_dim);
-    HIPCHK(ctx, launch_to_f32(ctx->d.dtype, d_cam, ctx->cvec, ctx->d.cam_dim, ctx->stream));
-    HIPCHK(ctx, hipMemcpyAsync(cam.data(), ctx->cvec, cam.size() * 4, hipMemcpyDeviceToHost, ctx->stream));
-    HIPCHK(ctx, hipStreamSynchronize(ctx->stream));
-  }
-  state_reset(st, cam.empty() ? nullptr : cam.data());
   const size_t bytes = (size_t)ctx->E * 4;
-  float *zc = ctx->r_zcur, *zh = ctx->r_zhat, *zn = ctx->r_znext;
-  HIPCHK(ctx, hipMemcpyAsync(zc, d_z, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  struct Sample {
+    wdc_state *st;
+    float *zc, *zh, *zn;
+    std::vector<double> pre;  // pass-1 statistics of zc, emitted by the kernel that wrote it
+  };
+  std::vector<Sample> sm(B);
+  for (int b = 0; b < B; ++b) {
+    wdc_state *st = states[b];
+    std::vector<float> cam;
+    const void *cb = d_cam ? d_cam[b] : nullptr;
+    if (cb && ctx->d.cam_dim > 0) {
+      cam.resize(ctx->d.cam_dim);
+      HIPCHK(ctx, launch_to_f32(ctx->d.dtype, cb, ctx->cvec, ctx->d.cam_dim, ctx->stream));
+      HIPCHK(ctx, hipMemcpyAsync(cam.data(), ctx->cvec, cam.size() * 4, hipMemcpyDeviceToHost, ctx->stream));
+      HIPCHK(ctx, hipStreamSynchronize(ctx->stream));
+    }
+    state_reset(st, cam.empty() ? nullptr : cam.data());
+    sm[b] = Sample{st, st->rz[0], st->rz[1], st->rz[2], {}};
+    HIPCHK(ctx, hipMemcpyAsync(sm[b].zc, d_z[b], bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  }
   wdc_step_log tmp;
-  std::vector<double> pre;  // pass-1 statistics of zc, emitted by the kernel that wrote it
+  std::vector<int> ex;
+  std::vector<const float *> zs;
+  std::vector<const void *> cs, ts, ms;
+  std::vector<float *> vs;
   for (int k = 0; k < S; ++k) {
-    wdc_step_log *lg = h_log ? &h_log[k] : &tmp;
-    CHK(surrogate_step(st, zc, k, S, zh, lg, k > 0 ? pre.data() : nullptr));
-    pre_decision(st, k, S, mode, h_forced ? h_forced[k] : 0, lg);
-    if (st->pend_surrogate) {
-      post_surrogate(st, lg);
-      std::swap(zc, zh);
-      pre.swap(st->pre_obs);
-      h_schedule[k] = 1;
-    } else {
-      const float *v;
-      if (d_replay_v) {
-        v = d_replay_v + (size_t)k * ctx->E;
+    ex.clear();
+    for (int b = 0; b < B; ++b) {
+      Sample &q = sm[b];
+      wdc_step_log *lg = h_log ? &h_log[(size_t)b * S + k] : &tmp;
+      CHK(surrogate_step(q.st, q.zc, k, S, q.zh, lg, k > 0 ? q.pre.data() : nullptr));
+      pre_decision(q.st, k, S, mode, h_forced ? h_forced[(size_t)b * S + k] : 0, lg);
+      if (q.st->pend_surrogate) {
+        post_surrogate(q.st, lg);
+        std::swap(q.zc, q.zh);
+        q.pre.swap(q.st->pre_obs);
+        h_schedule[(size_t)b * S + k] = 1;
       } else {
-        CHK(dit_forward(ctx, zc, t_at(k, S), d_cond, d_text, d_cam, ctx->r_v));
-        v = ctx->r_v;
+        ex.push_back(b);
+        h_schedule[(size_t)b * S + k] = 0;
       }
-      CHK(post_exact(st, zc, v, zn, k, S, lg));
-      std::swap(zc, zn);
-      pre.swap(st->pre_post);
-      h_schedule[k] = 0;
+    }
+    if (ex.empty()) continue;
+    // exact subset: one batched F_theta call (or the recorded velocities)
+    if (!d_replay_v) {
+      zs.clear();
+      cs.clear();
+      ts.clear();
+      ms.clear();
+      vs.clear();
+      for (size_t j = 0; j < ex.size(); ++j) {
+        const int b = ex[j];
+        zs.push_back(sm[b].zc);
+        cs.push_back(d_cond ? d_cond[b] : nullptr);
+        ts.push_back(d_text ? d_text[b] : nullptr);
+        ms.push_back(d_cam ? d_cam[b] : nullptr);
+        vs.push_back(ctx->r_v + j * ctx->E);
+      }
+      CHK(dit_forward_batch(ctx, (int)ex.size(), zs.data(), t_at(k, S), cs.data(), ts.data(), ms.data(), vs.data()));
+    }
+    for (size_t j = 0; j < ex.size(); ++j) {
+      const int b = ex[j];
+      Sample &q = sm[b];
+      wdc_step_log *lg = h_log ? &h_log[(size_t)b * S + k] : &tmp;
+      const float *v = d_replay_v ? d_replay_v[b] + (size_t)k * ctx->E : ctx->r_v + j * ctx->E;
+      CHK(post_exact(q.st, q.zc, v, q.zn, k, S, lg));
+      std::swap(q.zc, q.zn);
+      q.pre.swap(q.st->pre_post);
     }
   }
-  HIPCHK(ctx, hipMemcpyAsync(d_z, zc, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  for (int b = 0; b < B; ++b) HIPCHK(ctx, hipMemcpyAsync(d_z[b], sm[b].zc, bytes, hipMemcpyDeviceToDevice, ctx->stream));
   HIPCHK(ctx, hipStreamSynchronize(ctx->stream));
   return WDC_OK;
+}
+
+wdc_status wdc_rollout(wdc_ctx *ctx, wdc_state *st, float *d_z, int32_t S, const void *d_cond, const void *d_text,
+                       const void *d_cam, int32_t mode, const uint8_t *h_forced, const float *d_replay_v,
+                       uint8_t *h_schedule, wdc_step_log *h_log) {
+  if (!ctx || !st || !d_z) return WDC_E_ARG;
+  return wdc_rollout_batch(ctx, &st, 1, &d_z, S, d_cond ? &d_cond : nullptr, d_text ? &d_text : nullptr,
+                           d_cam ? &d_cam : nullptr, mode, h_forced, d_replay_v ? &d_replay_v : nullptr, h_schedule,
+                           h_log);
+}
+
+wdc_status wdc_dit_forward_batch(wdc_ctx *ctx, int32_t B, const float *const *d_z, double t,
+                                 const void *const *d_cond, const void *const *d_text, const void *const *d_cam,
+                                 float *const *d_v) {
+  if (!ctx || !d_z || !d_v || B < 1) return WDC_E_ARG;
+  for (int b = 0; b < B; ++b)
+    if (!d_z[b] || !d_v[b]) return WDC_E_ARG;
+  if (ctx->d.n_seq + ctx->d.n_dual + ctx->d.n_single == 0) {
+    set_err(ctx, "model has no blocks");
+    return WDC_E_STATE;
+  }
+  return dit_forward_batch(ctx, B, d_z, t, d_cond, d_text, d_cam, d_v);
 }
 
 int64_t wdc_attn_pad(int64_t n) { return attn_pad(n); }
