@@ -45,6 +45,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
     ap.add_argument("--surrogate-steps", type=int, default=20)
     ap.add_argument("--no-surrogate", action="store_true", help="skip the standalone surrogate-kernel leg")
+    ap.add_argument("--no-batch", action="store_true", help="skip the batched-rollout leg")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="also run one plain device copy of this many bytes (hardware-counter calibration)")
     return ap.parse_args()
@@ -142,6 +143,41 @@ def surrogate_leg(wdc, synth, torch, dev, steps=24):
     del ctx, st, z, z0, base, vel, zhat
     torch.cuda.empty_cache()
     return res
+
+
+def batched_leg(wdc, synth, torch, dev, steps=20, batches=(1, 8)):
+    """Throughput of batched rollouts on the mid workload (8 blocks, D = 1024, 2,688
+    tokens, bf16): B independent all-exact rollouts of `steps` denoising steps, F_theta
+    evaluated once per step for the whole batch, against B = 1."""
+    import dataclasses
+    cfg = synth.get_config("mid")
+    bmax = max(batches)
+    ctx = wdc.Context(cfg, device=str(dev), max_batch=bmax)
+    ctx.init_random_weights(seed=7, std=0.02)
+    inp = [synth.gen_inputs(dataclasses.replace(cfg, seed=cfg.seed + b)) for b in range(bmax)]
+    z0 = [torch.from_numpy(i["z_T"]).to(dev) for i in inp]
+    cond = [ctx.to_device(i["cond"]) for i in inp]
+    states = [ctx.new_state() for _ in range(bmax)]
+    out = {"workload": f"mid: {cfg.n_blocks} blocks, D={cfg.hidden}, {cfg.n_tokens} tokens, latent "
+                       f"{'x'.join(map(str, cfg.latent))}; all-exact rollouts of {steps} steps", "runs": []}
+    base = None
+    for B in batches:
+        zs = [z.clone() for z in z0[:B]]
+        ctx.rollout_batch(states[:B], zs, steps, cond[:B], mode=wdc.MODE_ALL_EXACT)      # warm-up
+        zs = [z.clone() for z in z0[:B]]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ctx.rollout_batch(states[:B], zs, steps, cond[:B], mode=wdc.MODE_ALL_EXACT)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        sps = B * steps / dt
+        base = base or sps
+        out["runs"].append({"batch": B, "seconds": round(dt, 4), "denoising_steps_per_s": round(sps, 1),
+                            "tflops": round(B * steps * cfg.flops_per_forward() / dt / 1e12, 1),
+                            "speedup_vs_batch1": round(sps / base, 2)})
+    del ctx, states, z0, cond
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -271,6 +307,9 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_surrogate:
         out["surrogate_kernels"] = surrogate_leg(wdc, synth, torch, dev)
+    if not args.no_batch:
+        log("batched rollouts (mid workload) ...")
+        out["batched_rollout"] = batched_leg(wdc, synth, torch, dev)
     if args.copy_probe > 0:
         src = torch.empty(args.copy_probe // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
