@@ -234,16 +234,35 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
     const float gv = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
+      const int64_t rb = m0 + wm * (BM / WM) + i * 32 + 4 * lg;   // row of element e: rb + 8 (e / 4) + e % 4
+      if (EPI == EPI_GATE_RES && m0 + wm * (BM / WM) + i * 32 + 32 <= g.m) {
+        // whole 32-row tile inside m (uniform per wave): read its 16 residual values,
+        // then update them, with no per-element branch (vmcnt also counts stores, so
+        // a guarded store per element would serialise every read-modify-write)
+        float *xc = (float *)g.c + rb * g.ldc + col;
+        float xr[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) xr[e] = xc[(8 * (e / 4) + (e % 4)) * g.ldc];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = xr[e] + gv * (acc[i][j][e] + bv);
+        continue;
+      }
+      if (EPI == EPI_GATE_RES) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int64_t row = rb + 8 * (e / 4) + (e % 4);
+          if (row < g.m) ((float *)g.c)[row * g.ldc + col] += gv * (acc[i][j][e] + bv);
+        }
+        continue;
+      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t row = m0 + wm * (BM / WM) + i * 32 + 8 * (e / 4) + 4 * lg + (e % 4);
+        const int64_t row = rb + 8 * (e / 4) + (e % 4);
         if (row >= g.m) continue;
         const float v = acc[i][j][e] + bv;
         const int64_t o = row * g.ldc + col;
         if (EPI == EPI_STORE || EPI == EPI_GELU)
           ((bf16_t *)g.c)[o] = f2bf(epi_act<EPI>(v));
-        else if (EPI == EPI_GATE_RES)
-          ((float *)g.c)[o] += gv * v;
         else
           ((float *)g.c)[o] = v;
       }
