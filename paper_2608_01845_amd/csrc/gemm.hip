@@ -126,6 +126,11 @@ __device__ __forceinline__ float epi_act(float v) {
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   using C = Cfg<BM, BN, WM, WN>;
+  // bf16 outputs: compute C^T tiles (weight fragment as the MFMA A operand) so a
+  // lane holds 4 consecutive columns of one row (8-byte stores); float32 outputs
+  // keep C tiles, whose lanes cover 32 consecutive columns of two rows (a full
+  // 128-byte line per read-modify-write instruction)
+  constexpr bool TR = EPI == EPI_STORE || EPI == EPI_GELU;
   const GemmArgs g = batch_entry<bf16_t>(g0);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char *sA = smem;                      // [2][BM][128 B]
@@ -218,53 +223,88 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
       for (int i = 0; i < C::TM; ++i)
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0)
+                         : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     __syncthreads();
   }
 #undef WDC_GEMM_LOAD
 
-  // epilogue: lane holds column lr of each 32x32 tile, rows 8*(e/4) + 4*lg + e%4
   const bf16_t *bias = (const bf16_t *)g.bias;
+  if constexpr (TR) {
+    // bf16 output: lane (lr, lg) of tile (i, j) holds row lr of the 32x32 output
+    // tile and, in accumulator entries 4q..4q+3, the four consecutive columns
+    // 8q + 4lg + 0..3, stored as one 8-byte group
 #pragma unroll
-  for (int j = 0; j < C::TN; ++j) {
-    const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
-    const float bv = bias ? bf2f(bias[col]) : 0.f;
-    const float gv = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
+    for (int j = 0; j < C::TN; ++j) {
+      const int64_t cb = n0 + wn * (BN / WN) + j * 32 + 4 * lg;   // column of group q: cb + 8 q
+      float bq[4][4];                                               // bias of the lane's 16 columns
 #pragma unroll
-    for (int i = 0; i < C::TM; ++i) {
-      const int64_t rb = m0 + wm * (BM / WM) + i * 32 + 4 * lg;   // row of element e: rb + 8 (e / 4) + e % 4
-      if (EPI == EPI_GATE_RES && m0 + wm * (BM / WM) + i * 32 + 32 <= g.m) {
-        // whole 32-row tile inside m (uniform per wave): read its 16 residual values,
-        // then update them, with no per-element branch (vmcnt also counts stores, so
-        // a guarded store per element would serialise every read-modify-write)
-        float *xc = (float *)g.c + rb * g.ldc + col;
-        float xr[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) xr[e] = xc[(8 * (e / 4) + (e % 4)) * g.ldc];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = xr[e] + gv * (acc[i][j][e] + bv);
-        continue;
+      for (int q = 0; q < 4; ++q) {
+        if (bias) {
+          const uint2 bw = *(const uint2 *)(bias + cb + 8 * q);
+          bq[q][0] = bf2f((bf16_t)(bw.x & 0xffff));
+          bq[q][1] = bf2f((bf16_t)(bw.x >> 16));
+          bq[q][2] = bf2f((bf16_t)(bw.y & 0xffff));
+          bq[q][3] = bf2f((bf16_t)(bw.y >> 16));
+        } else {
+          bq[q][0] = bq[q][1] = bq[q][2] = bq[q][3] = 0.f;
+        }
       }
-      if (EPI == EPI_GATE_RES) {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        const int64_t row = m0 + wm * (BM / WM) + i * 32 + lr;
+        if (row >= g.m) continue;
+        bf16_t *out = (bf16_t *)g.c + row * g.ldc + cb;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t w0 = (uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 0] + bq[q][0])) |
+                              ((uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 1] + bq[q][1])) << 16);
+          const uint32_t w1 = (uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 2] + bq[q][2])) |
+                              ((uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 3] + bq[q][3])) << 16);
+          *(uint2 *)(out + 8 * q) = make_uint2(w0, w1);
+        }
+      }
+    }
+  } else {
+    // float32 output: lane holds column lr of each 32x32 tile, rows
+    // 8 (e / 4) + 4 lg + e % 4; 32 lanes cover one 128-byte line per row
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
+      const float bv = bias ? bf2f(bias[col]) : 0.f;
+      const float gv = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        const int64_t rb = m0 + wm * (BM / WM) + i * 32 + 4 * lg;   // row of element e: rb + 8 (e / 4) + e % 4
+        float *xc = (float *)g.c + rb * g.ldc + col;
+        if (m0 + wm * (BM / WM) + i * 32 + 32 <= g.m) {
+          // whole 32-row tile inside m (uniform per wave): no per-element guard, so
+          // the residual reads go out together (vmcnt also counts stores, and a
+          // guarded store per element would serialise every read-modify-write)
+          if (EPI == EPI_GATE_RES) {
+            float xr[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) xr[e] = xc[(8 * (e / 4) + (e % 4)) * g.ldc];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = xr[e] + gv * (acc[i][j][e] + bv);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = acc[i][j][e] + bv;
+          }
+          continue;
+        }
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int64_t row = rb + 8 * (e / 4) + (e % 4);
-          if (row < g.m) ((float *)g.c)[row * g.ldc + col] += gv * (acc[i][j][e] + bv);
+          if (row >= g.m) continue;
+          float *x = (float *)g.c + row * g.ldc + col;
+          if (EPI == EPI_GATE_RES)
+            *x += gv * (acc[i][j][e] + bv);
+          else
+            *x = acc[i][j][e] + bv;
         }
-        continue;
-      }
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t row = rb + 8 * (e / 4) + (e % 4);
-        if (row >= g.m) continue;
-        const float v = acc[i][j][e] + bv;
-        const int64_t o = row * g.ldc + col;
-        if (EPI == EPI_STORE || EPI == EPI_GELU)
-          ((bf16_t *)g.c)[o] = f2bf(epi_act<EPI>(v));
-        else
-          ((float *)g.c)[o] = v;
       }
     }
   }
@@ -296,7 +336,10 @@ void set_lds_limit() {
 
 hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
-  const bool aligned = ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0;
+  // the MFMA kernels read 16-byte operand chunks and write 4-column output groups
+  const bool aligned = ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0 &&
+                       (uintptr_t)g.c % 16 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.bias % 8 == 0 &&
+                       (uintptr_t)g.gate % 16 == 0 && (g.batch <= 1 || (g.a_bs % 8 == 0 && g.c_bs % 4 == 0 && g.gate_bs % 4 == 0));
   if (dtype == 1 && aligned) {
     static bool init = false;
     if (!init) {
