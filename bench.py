@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--surrogate-steps", type=int, default=20)
     ap.add_argument("--no-surrogate", action="store_true", help="skip the standalone surrogate-kernel leg")
     ap.add_argument("--no-batch", action="store_true", help="skip the batched-rollout leg")
+    ap.add_argument("--surrogate-only", action="store_true",
+                    help="run only the surrogate-kernel leg (16x33x90x160 latent) and print its JSON")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="also run one plain device copy of this many bytes (hardware-counter calibration)")
     return ap.parse_args()
@@ -194,6 +196,9 @@ def main():
     cfg = synth.get_config(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.surrogate_only:
+        print(json.dumps({"surrogate_kernels": surrogate_leg(wdc, synth, torch, dev)}), flush=True)
+        return
     S = cfg.steps
     log(f"workload {cfg.name}: {cfg.n_blocks} blocks, N={cfg.n_tokens}, D={cfg.hidden}, {cfg.heads}x{cfg.head_dim}")
     ctx = wdc.Context(cfg, device="cuda:0")

@@ -289,11 +289,91 @@ __global__ void k_copy_rows(const float *src, int64_t lds, float *dst, int64_t l
 inline unsigned nblk(int64_t n, int t) { return (unsigned)((n + t - 1) / t); }
 }  // namespace
 
+// Vector form (d % 4 == 0, 16-byte aligned rows): thread t owns the float4
+// groups t, t + 256, ... of the row; bf16 output goes out as 8-byte groups.
+template <typename T>
+__device__ __forceinline__ void st4(T *p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void st4<bf16_t>(bf16_t *p, float a, float b, float c, float d) {
+  *(uint2 *)p = make_uint2((uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16), (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16));
+}
+template <>
+__device__ __forceinline__ void st4<float>(float *p, float a, float b, float c, float d) {
+  *(float4 *)p = make_float4(a, b, c, d);
+}
+
+template <typename T, int NV4>
+__global__ __launch_bounds__(256) void k_ln_mod4(const float *__restrict__ x, int64_t ldx, T *__restrict__ h,
+                                                int64_t ldh, LnRows lr, int d, const float *__restrict__ shift,
+                                                const float *__restrict__ scale) {
+  __shared__ float red[8];
+  const int64_t i = blockIdx.x;
+  const int64_t smp = i / lr.rps;
+  const int64_t r = smp * lr.sstride + i % lr.rps;
+  shift += smp * lr.mstride;
+  scale += smp * lr.mstride;
+  const float4 *xr = (const float4 *)(x + r * ldx);
+  const int d4 = d >> 2;
+  float4 v[NV4];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV4; ++k) {
+    const int c = threadIdx.x + k * 256;
+    v[k] = c < d4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    s += (v[k].x + v[k].y) + (v[k].z + v[k].w);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  s = warp_sum(s);
+  if (lane == 0) red[w] = s;
+  __syncthreads();
+  const float mean = (red[0] + red[1] + red[2] + red[3]) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV4; ++k) {
+    const int c = threadIdx.x + k * 256;
+    if (c < d4) {
+      const float a = v[k].x - mean, b = v[k].y - mean, e = v[k].z - mean, f = v[k].w - mean;
+      q += (a * a + b * b) + (e * e + f * f);
+    }
+  }
+  q = warp_sum(q);
+  if (lane == 0) red[4 + w] = q;
+  __syncthreads();
+  const float var = (red[4] + red[5] + red[6] + red[7]) / (float)d;
+  const float rstd = rsqrtf(var + 1e-6f);
+  T *hr = h + r * ldh;
+#pragma unroll
+  for (int k = 0; k < NV4; ++k) {
+    const int c = threadIdx.x + k * 256;
+    if (c < d4) {
+      const float4 sh = ((const float4 *)shift)[c], sc = ((const float4 *)scale)[c];
+      st4<T>(hr + 4 * c, (v[k].x - mean) * rstd * (1.f + sc.x) + sh.x, (v[k].y - mean) * rstd * (1.f + sc.y) + sh.y,
+             (v[k].z - mean) * rstd * (1.f + sc.z) + sh.z, (v[k].w - mean) * rstd * (1.f + sc.w) + sh.w);
+    }
+  }
+}
+
 hipError_t launch_ln_mod(int dtype, const float *x, int64_t ldx, void *h, int64_t ldh, const LnRows &r, int d,
                          const float *shift, const float *scale, hipStream_t s) {
   if (r.rows <= 0) return hipSuccess;
   if (d > 16 * 256 || r.rps <= 0 || r.sstride < r.rps) return hipErrorInvalidValue;
   dim3 g((unsigned)r.rows), b(256);
+  const bool vec = d % 4 == 0 && ldx % 4 == 0 && ldh % 4 == 0 && r.mstride % 4 == 0 && (uintptr_t)x % 16 == 0 &&
+                   (uintptr_t)h % 16 == 0 && (uintptr_t)shift % 16 == 0 && (uintptr_t)scale % 16 == 0;
+  if (vec) {
+    if (dtype == 1) {
+      if (d <= 4 * 256)
+        hipLaunchKernelGGL((k_ln_mod4<bf16_t, 1>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, r, d, shift, scale);
+      else
+        hipLaunchKernelGGL((k_ln_mod4<bf16_t, 4>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, r, d, shift, scale);
+    } else {
+      if (d <= 4 * 256)
+        hipLaunchKernelGGL((k_ln_mod4<float, 1>), g, b, 0, s, x, ldx, (float *)h, ldh, r, d, shift, scale);
+      else
+        hipLaunchKernelGGL((k_ln_mod4<float, 4>), g, b, 0, s, x, ldx, (float *)h, ldh, r, d, shift, scale);
+    }
+    return hipGetLastError();
+  }
   if (dtype == 1) {
     if (d <= 4 * 256)
       hipLaunchKernelGGL((k_ln_mod<bf16_t, 4>), g, b, 0, s, x, ldx, (bf16_t *)h, ldh, r, d, shift, scale);
