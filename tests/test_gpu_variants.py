@@ -128,3 +128,27 @@ def test_periodic_secant_tiny_dit_matches_oracle():
     assert sched == ref.schedule == [0, 1, 1, 0, 1, 1, 0, 1]
     compare(logs, ref.log)
     assert rel_l2(z.cpu().numpy(), ref.z) <= TOL_F32
+
+
+@pytest.mark.parametrize("capacity", [1, 8])
+def test_bank_capacity_extremes(capacity):
+    """FIFO of one record (every insert replaces it) and of the largest capacity the
+    kernels take; 30 steps so the 8-slot bank wraps around."""
+    mode = "forced"
+    mask = [0 if k % 3 == 0 else 1 for k in range(30)]
+    run_variant(synth.get_config("tiny"), 30, dict(bank_capacity=capacity, theta_sim=-1.0), mode, forced=mask)
+
+
+@pytest.mark.parametrize("steps", [1, 2])
+def test_shortest_rollouts(steps):
+    """One step (always exact: empty bank) and two steps (the second may commit a
+    candidate built from a single record)."""
+    ref = run_variant(synth.get_config("tiny"), steps, dict(tau_risk=float("inf")), "forced",
+                      forced=[1] * steps)
+    assert ref.schedule[0] == 0
+
+
+def test_open_threshold_takes_every_available_step():
+    ref = run_variant(synth.get_config("tiny"), 20, dict(tau_risk=1e9, theta_sim=-1.0), "forced",
+                      forced=[1] * 20)
+    assert ref.schedule == [0 if k % 8 == 0 else 1 for k in range(20)]
