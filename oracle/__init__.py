@@ -13,9 +13,18 @@ Modules
   scheduler  the scheduler transition Psi_t of Eq. (1) (flow-matching Euler)
   surrogate  the latent dynamics surrogate G_t: Eq. (2)-(5)
   risk       the transition risk controller: Eq. (6)-(10)
-  rollout    the inference loop of Sec. 4.4 (exact anchors and surrogate steps)
+  rollout    the inference loop of Sec. 4.4 (exact anchors and surrogate steps),
+             with the periodic placement and surrogate variants of Sec. 5.4
+  diagnostics  the injection sweep of Observation 1 (Sec. 3) and the
+             correlation / false-safe statistics of Sec. 4.3
 
 Where the paper defers details to its supplementary material, the reading
 used is recorded in ``params.DEFAULTS`` and in the module docstrings.
+
+Parity unpinned: ``dit.dit_forward`` as a composed whole (each operation and
+block is pinned, but a random-init model has no value the paper fixes), and
+the numerical values the diagnostics produce on such a model (the paper's
+correlations and false-safe rates come from trained models); the diagnostics'
+own arithmetic is pinned.
 """
 from . import params, dit, scheduler, surrogate, risk, rollout  # noqa: F401
