@@ -738,17 +738,20 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp(AttnArgs a) {
   }
 }
 
-// Ping-pong kernel with four K and four V^T buffers: group A issues the loads
-// of K_{t+3} and V_{t+2} in step t, two steps before they are read, and at the
-// end of step t waits only for the loads of step t-1 (a partial vmcnt), so a
-// tile load has two full steps to land. The step loop is unrolled by four so
-// every LDS fragment address is a per-lane register plus an immediate offset.
-// Buffer reuse: K_{t+3} overwrites K_{t-1}, last read in the matrix phases of
-// step t-2; V_{t+2} overwrites V_{t-2}, last read in step t-2; both end at a
-// barrier before step t starts. Group B's prologue reads K_0 while group A's
-// first step fills buffers 3 (K) and 2 (V).
+// Reference-max ping-pong kernel (ppr), the default form: the 8-wave
+// ping-pong scheme above with four K and four V^T buffers and a lighter
+// vector phase.
+// Pipeline: group A issues the loads of K_{t+3} and V_{t+2} in step t, two
+// steps before they are read, and at the end of step t waits only for the
+// loads of step t-1 (a partial vmcnt), so a tile load has two full steps to
+// land. The step loop is unrolled by four so every LDS fragment address is a
+// per-lane register plus an immediate offset. Buffer reuse: K_{t+3}
+// overwrites K_{t-1}, last read in the matrix phases of step t-2; V_{t+2}
+// overwrites V_{t-2}, last read in step t-2; both end at a barrier before step
+// t starts. Group B's prologue reads K_0 while group A's first step fills
+// buffers 3 (K) and 2 (V).
 template <int HD>
-__device__ __forceinline__ void pp4_wait(int n_outstanding) {
+__device__ __forceinline__ void pp_wait4(int n_outstanding) {
   constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
   static_assert(KS + VS < 16, "vmcnt immediate");
   if (n_outstanding == KS + VS)
@@ -759,8 +762,109 @@ __device__ __forceinline__ void pp4_wait(int n_outstanding) {
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
 }
 
+// Vector phase: Q is scaled by sc = log2(e)/sqrt(HD) once, and -m enters the
+// QK contraction as one more 16-deep slice per 32-key half (ones on the key
+// side, -m as a bf16 pair on the query side), so the matrix phase hands over
+// S' = sc Q K^T - m and the vector phase is P = exp2(S'), its bf16 conversion
+// and the row sum of those bf16 values (the weights the PV product uses). m is
+// a reference, not a running max: the first tile's row max, moved to a row's
+// true max only when a lane's P sum over a tile exceeds 2^64 (then O and l are
+// rescaled and P recomputed). Any reference gives the same normalised result,
+// and P <= 2^64 keeps O and l far from float overflow.
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+constexpr float PPR_LIMIT = 0x1p64f;
+
+// -m as bf16 (hi, lo) in k-slots 0, 1 of lane group 0; m becomes -(hi + lo)
+__device__ __forceinline__ bf16x8 ppr_mfrag(float &m, int lg) {
+  const __bf16 hi = (__bf16)(-m);
+  const __bf16 lo = (__bf16)(-m - (float)hi);
+  m = -((float)hi + (float)lo);
+  bf16x8 f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (__bf16)0.f;
+  if (lg == 0) {
+    f[0] = hi;
+    f[1] = lo;
+  }
+  return f;
+}
+
 template <int HD>
-__global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
+__device__ __forceinline__ void ppr_qk(f32x16 (&S)[2], const char *k, const bf16x8 (&qf)[HD / 16],
+                                       const int (&kro)[HD / 16], const bf16x8 &ones, const bf16x8 &mf) {
+  f32x16 zero;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) zero[e] = 0.f;
+  S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, zero, 0, 0, 0);
+  S[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, zero, 0, 0, 0);
+#pragma unroll
+  for (int st_ = 0; st_ < HD / 16; ++st_)
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
+      S[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st_], S[kt], 0, 0, 0);
+    }
+}
+
+// row max over the tile's 64 keys (32 per lane, the rest in lane l ^ 32)
+__device__ __forceinline__ float ppr_rowmax(const f32x16 (&S)[2]) {
+  float mx = fmaxf(S[0][0], S[1][0]);
+#pragma unroll
+  for (int e = 1; e < 16; ++e) mx = fmaxf(mx, fmaxf(S[0][e], S[1][e]));
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float ppr_exp(const f32x16 (&S)[2], bf16x8 (&pf)[4]) {
+  const bf16x2_t one2 = {(__bf16)1.f, (__bf16)1.f};
+  float ls = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) pf[2 * kt + e / 8][e % 8] = (__bf16)__builtin_amdgcn_exp2f(S[kt][e]);
+#pragma unroll
+  for (int q = 0; q < 16; ++q)
+    ls = __builtin_amdgcn_fdot2_f32_bf16(bf16x2_t{pf[q / 4][2 * (q % 4)], pf[q / 4][2 * (q % 4) + 1]}, one2, ls,
+                                         false);
+  return ls;
+}
+
+// vector phase: keys >= valid masked, P = exp2(S'), l += sum P; a lane sum
+// above the limit moves the rows to their true max first
+template <int HD>
+__device__ __forceinline__ void ppr_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32x16 (&o)[HD / 32], float &m,
+                                            bf16x8 &mf, float &l, int valid, int lg) {
+  if (valid < KV) {                        // partial last tile only: a branch, not selects
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= valid) S[kt][e] = -1e30f;
+  }
+  float ls = ppr_exp(S, pf);
+  if (__any(ls > PPR_LIMIT)) {
+    const float mx = ppr_rowmax(S);
+    float mn = m + (mx > 8.f ? mx : 0.f);
+    mf = ppr_mfrag(mn, lg);
+    const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);
+    m = mn;
+    l *= alpha;
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[kt][e] -= d;
+    ls = ppr_exp(S, pf);
+  }
+  l += ls;
+}
+
+template <int HD>
+__global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   constexpr int QB = 256;                  // 8 waves x 32 queries
   constexpr int NB = 4;                    // K buffers and V^T buffers
   constexpr int K_BYTES = KV * HD * 2;
@@ -782,9 +886,14 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
   const int64_t qbase = (int64_t)qb * QB + wid * 32;
   const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
 
-  bf16x8 qf[HD / 16];
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+  bf16x8 qf[HD / 16];                      // Q^T scaled by sc: scores in log2 units
 #pragma unroll
-  for (int s = 0; s < HD / 16; ++s) qf[s] = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
+  for (int s = 0; s < HD / 16; ++s) {
+    const bf16x8 raw = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) qf[s][j] = (__bf16)((float)raw[j] * sc);
+  }
 
   const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
       (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
@@ -830,17 +939,40 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
   for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  float m = -1e30f, l = 0.f;
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+  bf16x8 ones;                             // key-side partner of the -m fragment
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones[j] = (__bf16)0.f;
+  if (lg == 0) {
+    ones[0] = (__bf16)1.f;
+    ones[1] = (__bf16)1.f;
+  }
+  float m = 0.f, l = 0.f;
+  bf16x8 mf = ppr_mfrag(m, lg);
   f32x16 S[2];
   bf16x8 pf[4];
-  pp_qk<HD>(S, smem, qf, kro);
-  pp_softmax<HD>(S, pf, o, m, l, sc, ntiles == 1 ? last_valid : KV, lg);
+  ppr_qk<HD>(S, smem, qf, kro, ones, mf);
+  {                                        // m = the first tile's row max
+    const int v0 = ntiles == 1 ? last_valid : KV;
+    if (v0 < KV) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= v0) S[kt][e] = -1e30f;
+    }
+    m = ppr_rowmax(S);
+    mf = ppr_mfrag(m, lg);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[kt][e] -= m;
+    l = ppr_exp(S, pf);
+  }
   if (!grp_a) __syncthreads();             // group B runs one phase behind
 
-  constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // MFMAs = fragment reads per matrix phase
+  constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per matrix phase
   // One tile step with compile-time buffer slot P = t % NB.
-#define WDC_PP4_STEP(P)                                                                          \
+#define WDC_PPR_STEP(P)                                                                          \
   {                                                                                              \
     const int t = t0 + (P);                                                                      \
     int issued = 0;                                                                              \
@@ -856,7 +988,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro);                                                 \
-    pp_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro);                                    \
+    ppr_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro, ones, mf);                         \
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);                                           \
     _Pragma("unroll") for (int i_ = 0; i_ < NMF - 4; ++i_) {                                     \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
@@ -865,20 +997,20 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
-    if (t + 1 < ntiles) pp_softmax<HD>(S, pf, o, m, l, sc, t + 2 < ntiles ? KV : last_valid, lg); \
-    if (grp_a) pp4_wait<HD>(issued);                                                             \
+    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mf, l, t + 2 < ntiles ? KV : last_valid, lg); \
+    if (grp_a) pp_wait4<HD>(issued);                                                             \
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
   }
   for (int t0 = 0; t0 < ntiles; t0 += NB) {
-    WDC_PP4_STEP(0)
+    WDC_PPR_STEP(0)
     if (t0 + 1 >= ntiles) break;
-    WDC_PP4_STEP(1)
+    WDC_PPR_STEP(1)
     if (t0 + 2 >= ntiles) break;
-    WDC_PP4_STEP(2)
+    WDC_PPR_STEP(2)
     if (t0 + 3 >= ntiles) break;
-    WDC_PP4_STEP(3)
+    WDC_PPR_STEP(3)
   }
-#undef WDC_PP4_STEP
+#undef WDC_PPR_STEP
   if (grp_a) __syncthreads();              // match group B's extra barrier
 
   const float lt = l + __shfl_xor(l, 32, 64);
@@ -899,17 +1031,18 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp4(AttnArgs a) {
 }
 
 template <int HD>
-hipError_t launch_bf16_pp4(const AttnArgs &a, hipStream_t s) {
+hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
   constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
   static bool init = false;
   if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16_pp4<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    hipFuncSetAttribute((const void *)k_attn_bf16_ppr<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     init = true;
   }
   dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16_pp4<HD>), grid, dim3(512), LDS, s, a);
+  hipLaunchKernelGGL((k_attn_bf16_ppr<HD>), grid, dim3(512), LDS, s, a);
   return hipGetLastError();
 }
+
 
 template <int HD>
 hipError_t launch_bf16_pp(const AttnArgs &a, hipStream_t s) {
@@ -956,11 +1089,10 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    // Default: the 8-wave ping-pong kernel, with four-deep tile buffers for
-    // hd 128 (3.9% faster at 67,576 tokens) and the 3 K / 2 V buffer form for
-    // hd 64 (equal within noise at 17,776 tokens, smaller LDS). WDC_ATTN_VARIANT
-    // selects other forms: 0 plain, 1 pipelined one block per CU, 2 pipelined
-    // two blocks per CU, 3 ping-pong 3 K / 2 V, 5 four-deep also for hd 64.
+    // Default: the 8-wave ping-pong kernel with four-deep tile buffers and the
+    // light vector phase (ppr). WDC_ATTN_VARIANT selects earlier forms for
+    // comparison: 0 plain, 1 pipelined one block per CU, 2 pipelined two blocks
+    // per CU, 3 ping-pong with 3 K / 2 V buffers and a running-max softmax.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 4;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
@@ -970,13 +1102,13 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
       if (variant == 1) return launch_bf16_pipe<128, 1, 1>(b, s);
       if (variant == 2) return launch_bf16_pipe<128, 1, 2>(b, s);
       if (variant == 3) return launch_bf16_pp<128>(b, s);
-      return launch_bf16_pp4<128>(b, s);
+      return launch_bf16_ppr<128>(b, s);
     }
     if (a.hd == 64) {
       if (variant == 0) return launch_bf16<64, 2>(b, s);
       if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(b, s);
-      if (variant == 5) return launch_bf16_pp4<64>(b, s);
-      return launch_bf16_pp<64>(b, s);
+      if (variant == 3) return launch_bf16_pp<64>(b, s);
+      return launch_bf16_ppr<64>(b, s);
     }
     return hipErrorInvalidValue;
   }

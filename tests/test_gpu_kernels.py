@@ -1,4 +1,6 @@
 """Kernel-level parity of the HIP path against the oracle (GPU)."""
+import math
+
 import numpy as np
 import pytest
 
@@ -47,11 +49,18 @@ def test_linear_matches_oracle(dtype, m, n, k):
 
 
 def _attn_inputs(ctx, heads, hd, n, seed, bf16):
-    torch = torch_cuda()
     rng = _rng(seed)
     q, k, v = (rng.standard_normal((heads, n, hd)) for _ in range(3))
     if bf16:
         q, k, v = (synth.round_bf16(x).astype(np.float64) for x in (q, k, v))
+    return (q, k, v), _attn_device(ctx, q, k, v, bf16)
+
+
+def _attn_device(ctx, q, k, v, bf16):
+    """Device copies in the kernel layouts: rows padded to the kernel's tile
+    multiple; bf16 V^T with the key order of the MFMA accumulator."""
+    torch_cuda()
+    heads, n, hd = q.shape
     npad = ctx.attn_pad(n)
     def pad(x):
         out = np.zeros((heads, npad, hd), np.float32)
@@ -68,10 +77,11 @@ def _attn_inputs(ctx, heads, hd, n, seed, bf16):
         vd = ctx.to_device(vt)
     else:
         vd = ctx.to_device(vp)
-    return (q, k, v), (qd, kd, vd)
+    return qd, kd, vd
 
 
-@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 700), (64, 61), (128, 512), (128, 1000), (128, 129)])
+@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 700), (64, 61), (128, 512), (128, 1000), (128, 129),
+                                        (128, 320), (128, 1111)])
 def test_attention_bf16_matches_oracle(head_dim, n):
     torch = torch_cuda()
     cfg = small_cfg("bf16", head_dim=head_dim)
@@ -86,6 +96,36 @@ def test_attention_bf16_matches_oracle(head_dim, n):
     err = rel_l2(got[:, : heads * head_dim], ref)
     assert err <= 1e-2, err
     assert np.all(got[:, heads * head_dim:] == 0)      # nothing written past the heads
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_attention_bf16_score_jumps(head_dim):
+    """Keys whose scores exceed every earlier key's by about 70 and then 140
+    log2 units: the bf16 kernel must move its reference max twice mid-row (its
+    P bound is 2^64 per lane sum), and a ragged last tile adds 14 more units."""
+    torch = torch_cuda()
+    cfg = small_cfg("bf16", head_dim=head_dim)
+    ctx = context(cfg, weights=False)
+    heads, n = cfg.heads, 700
+    rng = _rng(4242 + head_dim)
+    u = rng.standard_normal((heads, 1, head_dim))
+    q = u + 0.1 * rng.standard_normal((heads, n, head_dim))
+    k = rng.standard_normal((heads, n, head_dim))
+    # log2-unit score of key c*u against q ~ u: c |u|^2 log2(e) / sqrt(hd) ~ 70 c / c1
+    c1 = 70.0 * math.sqrt(head_dim) / (head_dim * math.log2(math.e))
+    for lo, hi, c in ((192, 448, c1), (448, 640, 2 * c1), (640, n, 2.2 * c1)):
+        k[:, lo:hi] = c * u + 0.1 * rng.standard_normal((heads, hi - lo, head_dim))
+    v = rng.standard_normal((heads, n, head_dim))
+    q, k, v = (synth.round_bf16(x).astype(np.float64) for x in (q, k, v))
+    qd, kd, vd = _attn_device(ctx, q, k, v, bf16=True)
+    ldo = heads * head_dim
+    out = torch.zeros((n, ldo), dtype=torch.bfloat16, device="cuda")
+    ctx.attention(qd, kd, vd, n, out, ldo)
+    got = out.float().cpu().numpy()
+    ref = dit.attention(q, k, v).transpose(1, 0, 2).reshape(n, ldo)
+    err = rel_l2(got, ref)
+    print("head_dim", head_dim, "rel_l2", err)
+    assert np.all(np.isfinite(got)) and err <= 1e-2, err
 
 
 @pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 77), (128, 100)])
