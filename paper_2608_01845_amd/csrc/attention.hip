@@ -738,18 +738,24 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_pp(AttnArgs a) {
   }
 }
 
-// Reference-max ping-pong kernel (ppr), the default form: the 8-wave
-// ping-pong scheme above with four K and four V^T buffers and a lighter
-// vector phase.
-// Pipeline: group A issues the loads of K_{t+3} and V_{t+2} in step t, two
-// steps before they are read, and at the end of step t waits only for the
-// loads of step t-1 (a partial vmcnt), so a tile load has two full steps to
+// Reference-max kernel (ppr), the default form. 8 wavefronts per block (two
+// per SIMD), 32 queries each, K/V tiles of 64 keys in four K and four V^T LDS
+// buffers. Every tile step of a wave is a matrix phase (O += V^T P^T for tile t,
+// S' for tile t+1, LDS fragment reads scheduled four ahead of the MFMAs)
+// followed by a vector phase (softmax of tile t+1); a step ends with the only
+// block barrier of the step. Within a step the waves run free, so the two waves
+// of a SIMD drift apart and one's vector phase overlaps the other's MFMAs (a
+// ping-pong with a barrier between the phases was 4.6% slower at hd 128 and 11%
+// at hd 64 on the same box).
+// Pipeline: group A (waves 0-3) issues the loads of K_{t+3} and V_{t+2} in step
+// t, two steps before they are read, and at the end of step t waits only for
+// the loads of step t-1 (a partial vmcnt), so a tile load has two full steps to
 // land. The step loop is unrolled by four so every LDS fragment address is a
-// per-lane register plus an immediate offset. Buffer reuse: K_{t+3}
-// overwrites K_{t-1}, last read in the matrix phases of step t-2; V_{t+2}
-// overwrites V_{t-2}, last read in step t-2; both end at a barrier before step
-// t starts. Group B's prologue reads K_0 while group A's first step fills
-// buffers 3 (K) and 2 (V).
+// per-lane register plus an immediate offset. Buffer reuse: step t reads V_t
+// and K_{t+1}; K_{t+3} overwrites K_{t-1}, last read in step t-2, and V_{t+2}
+// overwrites V_{t-2}, last read in step t-2; each wave drains its LDS reads
+// before the barrier that ends a step, so both were free two barriers before
+// the loads are issued.
 template <int HD>
 __device__ __forceinline__ void pp_wait4(int n_outstanding) {
   constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
@@ -968,7 +974,6 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
       for (int e = 0; e < 16; ++e) S[kt][e] -= m;
     l = ppr_exp(S, pf);
   }
-  if (!grp_a) __syncthreads();             // group B runs one phase behind
 
   constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per matrix phase
   // One tile step with compile-time buffer slot P = t % NB.
@@ -996,7 +1001,6 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
     }                                                                                            \
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
     __builtin_amdgcn_sched_barrier(0);                                                           \
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
     if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mf, l, t + 2 < ntiles ? KV : last_valid, lg); \
     if (grp_a) pp_wait4<HD>(issued);                                                             \
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
@@ -1011,7 +1015,6 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
     WDC_PPR_STEP(3)
   }
 #undef WDC_PPR_STEP
-  if (grp_a) __syncthreads();              // match group B's extra barrier
 
   const float lt = l + __shfl_xor(l, 32, 64);
   const float inv = 1.f / lt;
@@ -1089,8 +1092,8 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    // Default: the 8-wave ping-pong kernel with four-deep tile buffers and the
-    // light vector phase (ppr). WDC_ATTN_VARIANT selects earlier forms for
+    // Default: the 8-wave reference-max kernel with four-deep tile buffers and
+    // one barrier per tile (ppr). WDC_ATTN_VARIANT selects earlier forms for
     // comparison: 0 plain, 1 pipelined one block per CU, 2 pipelined two blocks
     // per CU, 3 ping-pong with 3 K / 2 V buffers and a running-max softmax.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 4;
