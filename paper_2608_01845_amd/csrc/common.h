@@ -101,6 +101,9 @@ struct GemmArgs {
   // writes c + z*c_bs (elements) with gate + z*gate_bs; batch 0 or 1 = one
   int batch;
   int64_t a_bs, c_bs, gate_bs;
+  // block-to-tile order of the MFMA kernels, chosen by launch_gemm: 0 groups
+  // of 8 M tiles, 1 one 8 x 4 tile rectangle per XCD per dispatch round
+  int order;
 };
 
 // dtype: 0 float32, 1 bfloat16

@@ -147,7 +147,17 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   const int first_m = gidx * group;
   const int gsize = min(m_tiles - first_m, group);
   int mt, nt;
-  if (gsize == group && n_tiles >= 24) {
+  if (g.order == 1) {
+    // Dispatch rounds of 256 blocks, one per CU; block id % 8 is its XCD. Round
+    // r gives XCD x chunk 8r + x: an 8 (M) x 4 (N) rectangle of tiles, one per
+    // block, so the 32 blocks an XCD runs together start together and share 8 A
+    // slices and 4 weight slices in its L2. Blocks past the last tile exit.
+    const int r = bid / 256, x = bid % 8, l = (bid / 8) % 32;
+    const int chunk = 8 * r + x, cpb = n_tiles / 4;
+    mt = 8 * (chunk / cpb) + l % 8;
+    nt = 4 * (chunk % cpb) + l / 8;
+    if (mt >= m_tiles) return;
+  } else if (gsize == group && n_tiles >= 24) {
     // Workgroups go to the 8 XCDs round robin (id % 8). Give each XCD a
     // contiguous run of n_tiles tiles of the group in (nt, mt) order: an
     // 8-row by n_tiles/8-column rectangle, so the ~32 blocks one XCD runs at
@@ -324,11 +334,30 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   }
 }
 
+// compute units of the current device (the rectangle order needs exactly 256)
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus[dev] = 0;
+  return cus[dev];
+}
+
 template <int BM, int BN, int WM, int WN>
-hipError_t launch_mfma(const GemmArgs &g, hipStream_t s) {
+hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
   using C = Cfg<BM, BN, WM, WN>;
+  GemmArgs g = g0;
   const int m_tiles = (int)((g.m + BM - 1) / BM), n_tiles = (int)(g.n / BN);
-  dim3 grid(m_tiles * n_tiles, 1, g.batch > 1 ? g.batch : 1), block(C::NT);
+  // WDC_GEMM_ORDER=0 keeps the older grouped order for comparison
+  static const int order = getenv("WDC_GEMM_ORDER") ? atoi(getenv("WDC_GEMM_ORDER")) : 1;
+  g.order = (order == 1 && BM == 256 && n_tiles % 4 == 0 && device_cus() == 256) ? 1 : 0;
+  int blocks = m_tiles * n_tiles;
+  if (g.order == 1) {
+    const int chunks = (m_tiles + 7) / 8 * (n_tiles / 4);
+    blocks = (chunks + 7) / 8 * 256;
+  }
+  dim3 grid(blocks, 1, g.batch > 1 ? g.batch : 1), block(C::NT);
   switch (g.epi) {
     case EPI_STORE: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GELU: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>), grid, block, C::LDS_BYTES, s, g); break;

@@ -30,7 +30,8 @@ def test_scheduler_step_matches_closed_form():
 
 @pytest.mark.parametrize("dtype,m,n,k", [
     ("bf16", 1000, 512, 3072), ("bf16", 600, 768, 1024), ("bf16", 300, 256, 128), ("bf16", 130, 384, 64),
-    ("bf16", 37, 64, 64), ("bf16", 1, 128, 256), ("f32", 300, 320, 96), ("f32", 5, 64, 256)])
+    ("bf16", 37, 64, 64), ("bf16", 1, 128, 256), ("bf16", 700, 2048, 256), ("bf16", 2100, 4096, 128),
+    ("f32", 300, 320, 96), ("f32", 5, 64, 256)])
 def test_linear_matches_oracle(dtype, m, n, k):
     torch = torch_cuda()
     cfg = synth.get_config("mid" if dtype == "bf16" else "tiny")
