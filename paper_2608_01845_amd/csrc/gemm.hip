@@ -388,12 +388,18 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
     if (!init) {
       set_lds_limit<256, 256, 2, 2>();
       set_lds_limit<256, 256, 2, 4>();
+      set_lds_limit<256, 256, 4, 4>();
       set_lds_limit<128, 128, 2, 2>();
       init = true;
     }
-    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
+    // 256 x 256 block tiles: 16 waves of 64 x 64 by default (four per SIMD; 2-6%
+    // faster than 8 waves of 128 x 64 on the N 3072-12288, K 3072 products, even
+    // at K 12288-15360). WDC_GEMM_VARIANT=1 selects 8 waves, 0 four waves of 128 x 128.
+    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 2;
     if (g.n % 256 == 0 && g.m >= 512)
-      return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s) : launch_mfma<256, 256, 2, 4>(g, s);
+      return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s)
+             : variant == 1 ? launch_mfma<256, 256, 2, 4>(g, s)
+                            : launch_mfma<256, 256, 4, 4>(g, s);
     if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
   }
   dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64), g.batch > 1 ? g.batch : 1), block(256);
