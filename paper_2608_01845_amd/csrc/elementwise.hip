@@ -140,6 +140,122 @@ __global__ __launch_bounds__(256) void k_v_transpose(QKVPrepArgs a) {
   }
 }
 
+// bf16 forms of the two kernels above with 16-byte accesses.
+// q/k: one thread per 8 consecutive elements (4 rotary pairs) of one head row;
+// the HD/8 threads of a head row are consecutive lanes of one wavefront, so the
+// RMS reduction is a butterfly over them. Same arithmetic per element as
+// k_qk_prep (float32, RMS scale, then rotation, one bf16 rounding).
+__device__ __forceinline__ void unpack8(const uint4 &u, float (&x)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack8(const float (&x)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_qk_prep8(QKVPrepArgs a) {
+  constexpr int TPH = HD / 8;              // threads per head row
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int c = (int)(gid % TPH);
+  const int64_t rh = gid / TPH;
+  const int h = (int)(rh % a.heads);
+  const int64_t r = rh / a.heads;
+  const bool live = r < a.rows;
+  const int64_t rr = live ? r : 0;
+  const bf16_t *src = (const bf16_t *)a.src + rr * a.ld + (int64_t)h * HD + 8 * c;
+  float q[8], k[8];
+  unpack8(*(const uint4 *)src, q);
+  unpack8(*(const uint4 *)(src + a.d), k);
+  if (a.qk_norm) {
+    float sq = 0.f, sk = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sq += q[e] * q[e];
+      sk += k[e] * k[e];
+    }
+#pragma unroll
+    for (int o = TPH / 2; o > 0; o >>= 1) {
+      sq += __shfl_xor(sq, o, 64);
+      sk += __shfl_xor(sk, o, 64);
+    }
+    const float rq = rsqrtf(sq / (float)HD + 1e-6f), rk = rsqrtf(sk / (float)HD + 1e-6f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      q[e] *= rq;
+      k[e] *= rk;
+    }
+  }
+  const int64_t j = a.row0 + rr;           // joint-sequence index
+  if (a.rope && j < a.n_video) {
+    const float4 *cs4 = (const float4 *)(a.rope + j * (HD / 2) + 4 * c);
+    const float4 c01 = cs4[0], c23 = cs4[1];
+    const float cs[8] = {c01.x, c01.y, c01.z, c01.w, c23.x, c23.y, c23.z, c23.w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const float co = cs[2 * p], si = cs[2 * p + 1];
+      float t0 = q[2 * p] * co - q[2 * p + 1] * si, t1 = q[2 * p] * si + q[2 * p + 1] * co;
+      q[2 * p] = t0;
+      q[2 * p + 1] = t1;
+      t0 = k[2 * p] * co - k[2 * p + 1] * si;
+      t1 = k[2 * p] * si + k[2 * p + 1] * co;
+      k[2 * p] = t0;
+      k[2 * p + 1] = t1;
+    }
+  }
+  if (!live) return;
+  const int64_t o = ((int64_t)h * a.n_pad + j) * HD + 8 * c;
+  *(uint4 *)((bf16_t *)a.q + o) = pack8(q);
+  *(uint4 *)((bf16_t *)a.k + o) = pack8(k);
+}
+
+// V^T through a 64-row LDS tile with 16-byte row reads and 16-byte writes of 8
+// consecutive V^T positions. Needs row0 % 16 == 0: then the key order of
+// vt_pos permutes tokens only inside each aligned group of 16 of this tile, and
+// output position p holds token vt_pos(p) (the permutation is its own
+// inverse). Groups of 16 with rows missing are written element by element,
+// valid tokens only (their other positions are padding, zeroed separately).
+template <int HD>
+__global__ __launch_bounds__(256) void k_v_transpose8(QKVPrepArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t tile[64][HD + 8];
+  const int h = blockIdx.y;
+  const int64_t r0 = (int64_t)blockIdx.x * 64;
+  for (int idx = threadIdx.x; idx < 64 * (HD / 8); idx += 256) {
+    const int rr = idx / (HD / 8), c = idx % (HD / 8);
+    const int64_t r = r0 + rr;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (r < a.rows) val = *(const uint4 *)((const bf16_t *)a.src + r * a.ld + 2 * a.d + (int64_t)h * HD + 8 * c);
+    *(uint4 *)&tile[rr][8 * c] = val;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < HD * 8; idx += 256) {
+    const int e = idx / 8, c = idx % 8;    // feature row, 8-position chunk of the tile
+    int tok[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) tok[i] = (int)vt_pos(8 * c + i);
+    bf16_t *dst = (bf16_t *)a.v + ((int64_t)h * HD + e) * a.n_pad + a.row0 + r0 + 8 * c;
+    const int64_t group_end = r0 + (8 * c / 16) * 16 + 16;   // rows this chunk's group needs
+    if (group_end <= a.rows) {
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w[i] = (uint32_t)tile[tok[2 * i]][e] | ((uint32_t)tile[tok[2 * i + 1]][e] << 16);
+      *(uint4 *)dst = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (r0 + tok[i] < a.rows) dst[i] = tile[tok[i]][e];
+    }
+  }
+}
+
 template <typename T>
 __global__ void k_qkv_pad(T *q, T *k, T *v, int heads, int hd, int64_t n, int64_t n_pad, int v_transposed) {
   const int64_t tail = n_pad - n;
@@ -394,11 +510,30 @@ hipError_t launch_qkv_prep(int dtype, const QKVPrepArgs &a, hipStream_t s) {
   const int64_t threads = a.rows * a.heads * (a.hd / 2);
   dim3 g(nblk(threads, 256)), b(256);
   if (dtype == 1) {
-    if (a.hd == 64)
+    // 16-byte forms when every row and head start is 16-byte aligned
+    const bool vec = (uintptr_t)a.src % 16 == 0 && a.ld % 8 == 0 && a.d % 8 == 0 && (uintptr_t)a.q % 16 == 0 &&
+                     (uintptr_t)a.k % 16 == 0 && (uintptr_t)a.v % 16 == 0 && a.n_pad % 8 == 0 &&
+                     (a.rope == nullptr || (uintptr_t)a.rope % 16 == 0);
+    if (vec) {
+      const dim3 g8(nblk(a.rows * a.heads * (a.hd / 8), 256));
+      if (a.hd == 64)
+        hipLaunchKernelGGL(k_qk_prep8<64>, g8, b, 0, s, a);
+      else
+        hipLaunchKernelGGL(k_qk_prep8<128>, g8, b, 0, s, a);
+    } else if (a.hd == 64) {
       hipLaunchKernelGGL((k_qk_prep<bf16_t, 32>), g, b, 0, s, a);
-    else
+    } else {
       hipLaunchKernelGGL((k_qk_prep<bf16_t, 64>), g, b, 0, s, a);
-    hipLaunchKernelGGL(k_v_transpose, dim3(nblk(a.rows, 64), a.heads), dim3(256), 0, s, a);
+    }
+    const dim3 gv(nblk(a.rows, 64), a.heads);
+    if (vec && a.row0 % 16 == 0) {
+      if (a.hd == 64)
+        hipLaunchKernelGGL(k_v_transpose8<64>, gv, dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL(k_v_transpose8<128>, gv, dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL(k_v_transpose, gv, dim3(256), 0, s, a);
+    }
   } else {
     if (a.hd == 64)
       hipLaunchKernelGGL((k_qk_prep<float, 32>), g, b, 0, s, a);
