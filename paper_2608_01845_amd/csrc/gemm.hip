@@ -103,8 +103,11 @@ struct Cfg {
   static constexpr int NT = 64 * WM * WN;       // threads
   static constexpr int TM = BM / WM / 32;       // 32x32 tiles per wave along M
   static constexpr int TN = BN / WN / 32;       // along N
-  static constexpr int A_CHUNKS = BM * 8 / NT;  // 1 KB stripes per wave per stage (= chunks per thread)
-  static constexpr int B_CHUNKS = BN * 8 / NT;
+  // the first LW waves (one per SIMD) issue the tile loads: with all 16 waves
+  // loading, the 16-wave kernel was 2-5% slower on the 13B products
+  static constexpr int LW = NT / 64 >= 4 ? 4 : NT / 64;
+  static constexpr int A_CHUNKS = BM * 8 / (64 * LW);  // 1 KB stripes per loading wave per stage
+  static constexpr int B_CHUNKS = BN * 8 / (64 * LW);
   static constexpr int LDS_BYTES = 2 * (BM + BN) * BK * 2;
 };
 
@@ -180,14 +183,14 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
 
   // Tiles go straight from HBM to LDS (buffer_load_dwordx4 ... lds: lane L of a
   // wavefront's load writes 16 bytes at LDS base + 16 L). Stripe s = 1 KB = 8
-  // tile rows; wave w loads stripes w, w + NW, w + 2 NW, ... so each lane fetches
+  // tile rows; loading wave w (of NW) loads stripes w, w + NW, w + 2 NW, ... so each lane fetches
   // row 8s + lane/8 and the logical chunk that the swizzle puts at physical
   // chunk lane%8 (the swizzle key (row >> 1) & 7 is the same for every stripe
   // of a wave since NW is even).
   // The A descriptor spans only this block's valid rows and every stripe's row
   // is in the VGPR offset, which the buffer range check covers: rows past m are
   // read as zero (the K offset rides in the SGPR offset and is always in range).
-  constexpr int NW = C::NT / 64;
+  constexpr int NW = C::LW;
   static_assert(NW % 2 == 0, "stripe swizzle assumes an even wave count");
   const int64_t rows_a = min((int64_t)BM, g.m - m0);
   const __amdgpu_buffer_rsrc_t a_desc = __builtin_amdgcn_make_buffer_rsrc(
@@ -221,10 +224,12 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
 #define WDC_GEMM_LOAD(buf, kt)                                                                     \
   {                                                                                                \
     const int kb_ = (kt) * BK * 2;                                                                 \
-    _Pragma("unroll") for (int i = 0; i < C::A_CHUNKS; ++i)                                         \
-        lds_load16(a_desc, sA + (buf) * BM * 128 + (i * NW + wu) * 1024, va[i], kb_);               \
-    _Pragma("unroll") for (int i = 0; i < C::B_CHUNKS; ++i)                                         \
-        lds_load16(b_desc, sB + (buf) * BN * 128 + (i * NW + wu) * 1024, vb, i * 8 * NW * (int)g.k * 2 + kb_); \
+    if (wu < NW) {                                                                                 \
+      _Pragma("unroll") for (int i = 0; i < C::A_CHUNKS; ++i)                                       \
+          lds_load16(a_desc, sA + (buf) * BM * 128 + (i * NW + wu) * 1024, va[i], kb_);             \
+      _Pragma("unroll") for (int i = 0; i < C::B_CHUNKS; ++i)                                       \
+          lds_load16(b_desc, sB + (buf) * BN * 128 + (i * NW + wu) * 1024, vb, i * 8 * NW * (int)g.k * 2 + kb_); \
+    }                                                                                              \
   }
 
   const int nk = (int)(g.k / BK);
