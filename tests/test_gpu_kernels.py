@@ -49,6 +49,29 @@ def test_linear_matches_oracle(dtype, m, n, k):
     assert err <= (4e-3 if dtype == "bf16" else TOL_F32), err
 
 
+def test_linear_large_product_rectangle_order():
+    """A product big enough for the XCD-rectangle block order (at least 64 chunks
+    of 8 x 4 tiles: 65 M tiles in 9 bands, the last one partial, x 32 N tiles),
+    with blocks past the last tile in the final dispatch round. Sampled rows,
+    including every row of the partial band, against the oracle."""
+    torch = torch_cuda()
+    cfg = synth.get_config("mid")
+    ctx = context(cfg, weights=False)
+    m, n, k = 16484, 8192, 64
+    rng = _rng(2024)
+    a = synth.stored(rng.standard_normal((m, k)), cfg.dtype)
+    w = synth.stored(rng.standard_normal((n, k)) * 0.05, cfg.dtype)
+    b = synth.stored(rng.standard_normal(n) * 0.1, cfg.dtype)
+    out = torch.empty((m, n), dtype=ctx.tdtype, device="cuda")
+    ctx.linear(ctx.to_device(a), ctx.to_device(w), ctx.to_device(b), out, m, n, k)
+    rows = np.unique(np.concatenate([rng.choice(16384, 96, replace=False), np.arange(16384, m)]))
+    got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    ref = dit.linear({"l.w": w, "l.b": b}, "l", a[rows].astype(np.float64))
+    err = rel_l2(got, ref)
+    print("rows", len(rows), "rel_l2", err)
+    assert err <= 4e-3, err
+
+
 def _attn_inputs(ctx, heads, hd, n, seed, bf16):
     rng = _rng(seed)
     q, k, v = (rng.standard_normal((heads, n, hd)) for _ in range(3))
