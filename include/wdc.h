@@ -266,7 +266,9 @@ wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, 
 /* ---------------------------------------------------------------- kernels exposed for tests and benchmarks */
 
 /* softmax(q k^T / sqrt(hd)) v over the full sequence, the attention of every
- * block. d_q, d_k: [heads, n_pad, hd]. d_vt for bf16: [heads, hd, n_pad], V
+ * block. bf16: float32 accumulation, q multiplied by log2(e)/sqrt(hd) and
+ * rounded to bf16 once in the kernel, attention weights rounded to bf16 before
+ * the product with v and the row sum. d_q, d_k: [heads, n_pad, hd]. d_vt for bf16: [heads, hd, n_pad], V
  * transposed with the keys of each aligned group of 16 stored in the order
  * 0-3, 8-11, 4-7, 12-15 (key j at column j with bits 2 and 3 swapped); for
  * float32: [heads, n_pad, hd]. n valid tokens, n_pad = wdc_attn_pad(n); rows
