@@ -273,7 +273,9 @@ wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, 
  * 0-3, 8-11, 4-7, 12-15 (key j at column j with bits 2 and 3 swapped); for
  * float32: [heads, n_pad, hd]. n valid tokens, n_pad = wdc_attn_pad(n); rows
  * (keys) >= n of q/k/v must be zero. d_o: [n, ldo], head h written at columns
- * [h*hd, (h+1)*hd). */
+ * [h*hd, (h+1)*hd); ldo >= heads*hd (else WDC_E_ARG). q, k, vt 16-byte
+ * aligned; for bf16 d_o 8-byte aligned and ldo a multiple of 4 (else
+ * WDC_E_ALIGN). */
 int64_t wdc_attn_pad(int64_t n);
 wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
                          int64_t ldo);

@@ -1459,7 +1459,10 @@ int64_t wdc_attn_pad(int64_t n) { return attn_pad(n); }
 wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
                          int64_t ldo) {
   if (!ctx || !d_q || !d_k || !d_vt || !d_o || n <= 0) return WDC_E_ARG;
+  if (ldo < (int64_t)ctx->H * ctx->hd) return WDC_E_ARG;     // heads would overlap and the last row overrun
   if (!aligned16(d_q) || !aligned16(d_k) || !aligned16(d_vt)) return WDC_E_ALIGN;
+  // bf16 rows leave as 8-byte groups of 4 columns
+  if (ctx->d.dtype == WDC_BF16 && ((uintptr_t)d_o % 8 != 0 || ldo % 4 != 0)) return WDC_E_ALIGN;
   AttnArgs a{};
   a.q = d_q;
   a.k = d_k;

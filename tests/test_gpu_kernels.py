@@ -152,6 +152,24 @@ def test_attention_bf16_score_jumps(head_dim):
     assert np.all(np.isfinite(got)) and err <= 1e-2, err
 
 
+def test_attention_rejects_bad_output_layout():
+    """ldo below heads*hd (rows would overlap and the last row overrun its
+    buffer) and a bf16 output stride that breaks the 8-byte column groups."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = small_cfg("bf16", head_dim=128)
+    ctx = context(cfg, weights=False)
+    heads, hd, n = cfg.heads, 128, 100
+    _, (qd, kd, vd) = _attn_inputs(ctx, heads, hd, n, seed=5, bf16=True)
+    out = torch.zeros((n, heads * hd + 8), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(wdc.WdcError):
+        ctx.attention(qd, kd, vd, n, out, heads * hd - 4)
+    with pytest.raises(wdc.WdcError):
+        ctx.attention(qd, kd, vd, n, out, heads * hd + 2)
+    ctx.attention(qd, kd, vd, n, out, heads * hd + 8)       # a valid stride still works
+    assert torch.isfinite(out.float()).all()
+
+
 @pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 77), (128, 100)])
 def test_attention_f32_matches_oracle(head_dim, n):
     torch = torch_cuda()
