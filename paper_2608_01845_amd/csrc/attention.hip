@@ -2,17 +2,18 @@
 // full (non-causal) spatio-temporal + text sequence.
 //
 // bf16 path (flash attention on the matrix cores, hd = 64 or 128):
-//  * each wavefront owns QT*32 queries; a 256-thread block owns 4*QT*32;
-//  * K tiles [64 keys][hd] and V^T tiles [hd][64 keys] are staged in LDS
-//    (double-buffered, next tile prefetched into registers);
+//  * 512-thread blocks of 256 queries, 32 per wavefront, two wavefronts per
+//    SIMD; K tiles [64 keys][hd] and V^T tiles [hd][64 keys] reach LDS by
+//    direct buffer loads, issued two tile steps ahead by four of the waves;
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the accumulator of a 32x32
-//    tile gives lane l one query (l % 32) and 16 keys, so the running max and
-//    sum of a query live in one lane and its partner l ^ 32 (one exchange);
+//    tile gives lane l one query (l % 32) and 16 keys, so a query's row
+//    statistics live in one lane and its partner l ^ 32 (one exchange);
 //  * O^T = V^T P^T reuses the S^T accumulators directly as the B operand: the
 //    8 accumulator values a lane holds for 16 consecutive keys become its 8
 //    bf16 k-values, and the V^T operand is read with the same key order, so P
 //    never goes through LDS;
-//  * online softmax in base 2 (scores pre-scaled by log2(e)/sqrt(hd)).
+//  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr, the
+//    default), or with a running max (k_attn_bf16_pp, kept for comparison).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
@@ -93,18 +94,6 @@ constexpr int KV = 64;                   // keys per LDS tile
 constexpr int RSRC_WORD3 = 0x00020000;   // raw buffer descriptor word 3
 constexpr int WAIT_VM0 = 0x0F70;         // s_waitcnt vmcnt(0), other counters untouched
 
-template <int HD, int QT>
-struct ACfg {
-  static constexpr int NS = HD / 16;            // k-steps of S = K Q^T
-  static constexpr int NH = HD / 32;            // 32-row tiles of O^T along hd
-  static constexpr int QW = 32 * QT;            // queries per wave
-  static constexpr int QB = 4 * QW;             // queries per block
-  static constexpr int K_CHUNKS = KV * HD / 8 / 256;   // 16-byte chunks per thread per K tile
-  static constexpr int V_CHUNKS = HD * KV / 8 / 256;
-  static constexpr int K_BYTES = KV * HD * 2;
-  static constexpr int LDS_BYTES = 2 * 2 * K_BYTES;  // 2 buffers x (K + V^T)
-};
-
 // LDS swizzles: 16 consecutive lanes read 16 different rows at one logical
 // chunk; the XOR spreads them over distinct bank groups of the 64 x 4-byte banks.
 // K tile: rows of HD bf16 = HD/8 16-byte chunks. hd = 128 (256-byte rows):
@@ -151,389 +140,6 @@ struct TileLoad {
     vvo = vr0 * (int)n_pad * 2 + (vps ^ ((vr0 >> 1) & 7)) * 16;
   }
 };
-
-template <int HD, int QT>
-__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
-  using C = ACfg<HD, QT>;
-  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  char *sK = smem;                     // [2][KV][HD]
-  char *sV = smem + 2 * C::K_BYTES;    // [2][HD][KV]
-
-  const int h = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qbase = (int64_t)blockIdx.x * C::QB + wid * C::QW;
-  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
-
-  // Q^T as B operand: lane holds query qbase + 32*qt + lr, hd [16s + 8lg, +8)
-  bf16x8 qf[QT][C::NS];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-    for (int s = 0; s < C::NS; ++s)
-      qf[qt][s] = *(const bf16x8 *)(Q + (qbase + 32 * qt + lr) * HD + 16 * s + 8 * lg);
-
-  // K rows and V^T rows of this head through buffer descriptors (byte offsets < 2^31)
-  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const int wu = __builtin_amdgcn_readfirstlane(wid);
-  const TileLoad<HD> tl(wu, lane, a.n_pad);
-  using TL = TileLoad<HD>;
-#define WDC_TILE_LOAD(KOFF, VOFF, tile)                                                             \
-  {                                                                                                 \
-    _Pragma("unroll") for (int i = 0; i < TL::K_STRIPES; ++i)                                       \
-        lds_load16(kdesc, sK + (KOFF) + wu * 1024 + i * 4096, tl.kvo, (tile) * KV * HD * 2 + i * 4096); \
-    _Pragma("unroll") for (int i = 0; i < TL::V_STRIPES; ++i)                                       \
-        lds_load16(vdesc, sV + (VOFF) + wu * 1024 + i * 4096, tl.vvo,                                \
-                   (tile) * KV * 2 + i * 32 * (int)a.n_pad * 2);                                     \
-  }
-
-  f32x16 o[C::NH][QT];
-#pragma unroll
-  for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][qt][e] = 0.f;
-  float m[QT], l[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m[qt] = -1e30f;
-    l[qt] = 0.f;
-  }
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);   // log2(e)/sqrt(hd)
-
-  // fragment read offsets
-  int kro[C::NS];
-#pragma unroll
-  for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
-
-  const int ntiles = (int)((a.n + KV - 1) / KV);
-  WDC_TILE_LOAD(0, 0, 0);
-  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const bool more = t + 1 < ntiles;
-    if (more) WDC_TILE_LOAD((buf ^ 1) * C::K_BYTES, (buf ^ 1) * C::K_BYTES, t + 1);
-    const char *k = sK + buf * C::K_BYTES, *v = sV + buf * C::K_BYTES;
-
-    // S^T = K Q^T: [2 key tiles][QT query tiles]
-    f32x16 s[2][QT];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[kt][qt][e] = 0.f;
-#pragma unroll
-    for (int st_ = 0; st_ < C::NS; ++st_) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          s[kt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][st_], s[kt][qt], 0, 0, 0);
-      }
-    }
-    // key of accumulator e of key tile kt: 32kt + 8(e/4) + 4lg + e%4
-    const int64_t k0 = (int64_t)t * KV;
-    if (k0 + KV > a.n) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (k0 + 32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= a.n) s[kt][qt][e] = -1e30f;
-    }
-    bool moved = false;
-    float msc[QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      float mx = s[0][qt][0];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m[qt], mx * sc);   // running max of the scaled scores
-      moved |= mn > m[qt];
-      msc[qt] = mn;
-    }
-    // rescale the running sums and outputs only when some query's max moved
-    if (__any(moved)) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        const float alpha = __builtin_amdgcn_exp2f(m[qt] - msc[qt]);
-        l[qt] *= alpha;
-#pragma unroll
-        for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
-      }
-    }
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      m[qt] = msc[qt];
-      float sum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][qt][e], sc, -msc[qt]));
-          s[kt][qt][e] = p;
-          sum += p;
-        }
-      l[qt] += sum;
-    }
-    // O^T += V^T P^T over 4 k-steps of 16 keys
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      bf16x8 pf[QT];
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pf[qt][e] = (__bf16)s[j >> 1][qt][8 * (j & 1) + e];
-#pragma unroll
-      for (int i = 0; i < C::NH; ++i) {
-        const char *vb = v + i * 32 * KV * 2;
-        const bf16x8 vf = *(const bf16x8 *)(vb + vro[j]);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qt], o[i][qt], 0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-    __syncthreads();
-  }
-#undef WDC_TILE_LOAD
-  // normalise and store: lane holds query 32qt + lr, hd 32i + 8(e/4) + 4lg + e%4
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);
-    const float inv = 1.f / lt;
-    const int64_t q = qbase + 32 * qt + lr;
-    if (q >= a.n) continue;
-    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
-#pragma unroll
-    for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * i + 8 * g4 + 4 * lg;
-        uint32_t w0 = (uint32_t)f2bf(o[i][qt][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 1] * inv) << 16);
-        uint32_t w1 = (uint32_t)f2bf(o[i][qt][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 3] * inv) << 16);
-        *(uint2 *)(O + d0) = make_uint2(w0, w1);
-      }
-  }
-}
-
-// Software-pipelined variant: K is staged one tile ahead of V, so S for tile
-// t+1 is issued on the matrix cores before the softmax of tile t runs on the
-// vector ALUs. LDS holds two K tiles and two V^T tiles:
-//   iteration t reads K_{t+1} (kbuf[(t+1)&1]) and V_t (vbuf[t&1]) and writes
-//   K_{t+2} into kbuf[t&1] (last read in iteration t-1) and V_{t+1} into
-//   vbuf[(t+1)&1] (last read in iteration t-1); one barrier per iteration.
-template <int HD, int QT, int MINB>
-__global__ __launch_bounds__(256, MINB) void k_attn_bf16_pipe(AttnArgs a) {
-  using C = ACfg<HD, QT>;
-  typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  char *sK = smem;                     // [2][KV][HD]
-  char *sV = smem + 2 * C::K_BYTES;    // [2][HD][KV]
-
-  // Workgroups are dispatched round-robin over the 8 XCDs (linear id mod 8).
-  // With xcd_order, XCD x walks heads x, x+8, ... so the blocks resident on one
-  // XCD at a time belong to one head and share its K/V tiles in that XCD's L2.
-  int h = blockIdx.y, qb = blockIdx.x;
-  if (a.xcd_order) {
-    const int id = blockIdx.x + blockIdx.y * gridDim.x;
-    const int li = id >> 3;
-    h = (id & 7) + 8 * (li / gridDim.x);
-    qb = li % gridDim.x;
-  }
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qbase = (int64_t)qb * C::QB + wid * C::QW;
-  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
-
-  bf16x8 qf[QT][C::NS];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-    for (int s = 0; s < C::NS; ++s)
-      qf[qt][s] = *(const bf16x8 *)(Q + (qbase + 32 * qt + lr) * HD + 16 * s + 8 * lg);
-
-  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const int wu = __builtin_amdgcn_readfirstlane(wid);
-  const TileLoad<HD> tl(wu, lane, a.n_pad);
-  using TL = TileLoad<HD>;
-  int kro[C::NS];
-#pragma unroll
-  for (int s = 0; s < C::NS; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
-
-  const int ntiles = (int)((a.n + KV - 1) / KV);
-  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
-
-#define WDC_LOAD_K(b, tile)                                                                          \
-  _Pragma("unroll") for (int i = 0; i < TL::K_STRIPES; ++i)                                          \
-      lds_load16(kdesc, sK + (b) * C::K_BYTES + wu * 1024 + i * 4096, tl.kvo, (tile) * KV * HD * 2 + i * 4096)
-#define WDC_LOAD_V(b, tile)                                                                          \
-  _Pragma("unroll") for (int i = 0; i < TL::V_STRIPES; ++i)                                          \
-      lds_load16(vdesc, sV + (b) * C::K_BYTES + wu * 1024 + i * 4096, tl.vvo,                              \
-                 (tile) * KV * 2 + i * 32 * (int)a.n_pad * 2)
-
-  // prologue: K_0, V_0, K_1
-  WDC_LOAD_K(0, 0);
-  WDC_LOAD_V(0, 0);
-  if (ntiles > 1) WDC_LOAD_K(1, 1);
-  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-  __syncthreads();
-
-  f32x16 o[C::NH][QT];
-#pragma unroll
-  for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][qt][e] = 0.f;
-  float m[QT], l[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m[qt] = -1e30f;
-    l[qt] = 0.f;
-  }
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
-
-  f32x16 s[2][QT];
-  auto qk = [&](f32x16(&dst)[2][QT], const char *k) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) dst[kt][qt][e] = 0.f;
-#pragma unroll
-    for (int st_ = 0; st_ < C::NS; ++st_)
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          dst[kt][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qt][st_], dst[kt][qt], 0, 0, 0);
-      }
-  };
-  qk(s, sK);
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const bool more_k = t + 2 < ntiles, more_v = t + 1 < ntiles;
-    if (more_k) WDC_LOAD_K(buf, t + 2);          // kbuf[t&1] held K_t, read last iteration
-    if (more_v) WDC_LOAD_V(buf ^ 1, t + 1);      // vbuf[(t+1)&1] held V_{t-1}, read last iteration
-    f32x16 sn[2][QT];
-    if (more_v) qk(sn, sK + ((t + 1) & 1) * C::K_BYTES);
-
-    if (!more_v && last_valid < KV) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= last_valid) s[kt][qt][e] = -1e30f;
-    }
-    bool moved = false;
-    float msc[QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      float mx = s[0][qt][0];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m[qt], mx * sc);
-      moved |= mn > m[qt];
-      msc[qt] = mn;
-    }
-    if (__any(moved)) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        const float alpha = __builtin_amdgcn_exp2f(m[qt] - msc[qt]);
-        l[qt] *= alpha;
-#pragma unroll
-        for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[i][qt][e] *= alpha;
-      }
-    }
-    bf16x8 pf[4][QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      m[qt] = msc[qt];
-      float sum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][qt][e], sc, -msc[qt]));
-          sum += p;
-          pf[2 * kt + e / 8][qt][e % 8] = (__bf16)p;
-        }
-      l[qt] += sum;
-    }
-    const char *v = sV + (t & 1) * C::K_BYTES;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-#pragma unroll
-      for (int i = 0; i < C::NH; ++i) {
-        const char *vb = v + i * 32 * KV * 2;
-        const bf16x8 vf = *(const bf16x8 *)(vb + vro[j]);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          o[i][qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j][qt], o[i][qt], 0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-    __syncthreads();
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) s[kt][qt] = sn[kt][qt];
-  }
-#undef WDC_LOAD_K
-#undef WDC_LOAD_V
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);
-    const float inv = 1.f / lt;
-    const int64_t q = qbase + 32 * qt + lr;
-    if (q >= a.n) continue;
-    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
-#pragma unroll
-    for (int i = 0; i < C::NH; ++i)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * i + 8 * g4 + 4 * lg;
-        uint32_t w0 = (uint32_t)f2bf(o[i][qt][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 1] * inv) << 16);
-        uint32_t w1 = (uint32_t)f2bf(o[i][qt][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][qt][4 * g4 + 3] * inv) << 16);
-        *(uint2 *)(O + d0) = make_uint2(w0, w1);
-      }
-  }
-}
 
 // Ping-pong variant: 8 wavefronts per block in two groups of 4 (waves w and
 // w + 4 share a SIMD). Every tile step has an MFMA phase (O += V^T P^T for tile
@@ -1060,32 +666,6 @@ hipError_t launch_bf16_pp(const AttnArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int HD, int QT, int MINB>
-hipError_t launch_bf16_pipe(const AttnArgs &a, hipStream_t s) {
-  using C = ACfg<HD, QT>;
-  static bool init = false;
-  if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16_pipe<HD, QT, MINB>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                        C::LDS_BYTES);
-    init = true;
-  }
-  dim3 grid((unsigned)((a.n + C::QB - 1) / C::QB), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16_pipe<HD, QT, MINB>), grid, dim3(256), C::LDS_BYTES, s, a);
-  return hipGetLastError();
-}
-
-template <int HD, int QT>
-hipError_t launch_bf16(const AttnArgs &a, hipStream_t s) {
-  using C = ACfg<HD, QT>;
-  static bool init = false;
-  if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16<HD, QT>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-    init = true;
-  }
-  dim3 grid((unsigned)((a.n + C::QB - 1) / C::QB), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16<HD, QT>), grid, dim3(256), C::LDS_BYTES, s, a);
-  return hipGetLastError();
-}
 }  // namespace
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
@@ -1093,26 +673,14 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
     // Default: the 8-wave reference-max kernel with four-deep tile buffers and
-    // one barrier per tile (ppr). WDC_ATTN_VARIANT selects earlier forms for
-    // comparison: 0 plain, 1 pipelined one block per CU, 2 pipelined two blocks
-    // per CU, 3 ping-pong with 3 K / 2 V buffers and a running-max softmax.
+    // one barrier per tile (ppr). WDC_ATTN_VARIANT=3 selects the earlier
+    // ping-pong form (3 K / 2 V buffers, running-max softmax) for comparison.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 4;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
     b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
-    if (a.hd == 128) {
-      if (variant == 0) return launch_bf16<128, 1>(b, s);
-      if (variant == 1) return launch_bf16_pipe<128, 1, 1>(b, s);
-      if (variant == 2) return launch_bf16_pipe<128, 1, 2>(b, s);
-      if (variant == 3) return launch_bf16_pp<128>(b, s);
-      return launch_bf16_ppr<128>(b, s);
-    }
-    if (a.hd == 64) {
-      if (variant == 0) return launch_bf16<64, 2>(b, s);
-      if (variant == 1 || variant == 2) return launch_bf16_pipe<64, 2, 1>(b, s);
-      if (variant == 3) return launch_bf16_pp<64>(b, s);
-      return launch_bf16_ppr<64>(b, s);
-    }
+    if (a.hd == 128) return variant == 3 ? launch_bf16_pp<128>(b, s) : launch_bf16_ppr<128>(b, s);
+    if (a.hd == 64) return variant == 3 ? launch_bf16_pp<64>(b, s) : launch_bf16_ppr<64>(b, s);
     return hipErrorInvalidValue;
   }
   dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);
