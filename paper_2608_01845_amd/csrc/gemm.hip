@@ -90,6 +90,12 @@ __global__ __launch_bounds__(256) void k_gemm_simple(GemmArgs g0) {
 constexpr int BK = 64;  // K per LDS stage: one 128-byte row of bf16 per tile row
 constexpr int RSRC_WORD3 = 0x00020000;  // raw buffer: 32-bit data format, no swizzle
 constexpr int WAIT_VM0 = 0x0F70;        // s_waitcnt vmcnt(0), other counters untouched
+constexpr int WAIT_LGKM0 = 0xC07F;      // s_waitcnt lgkmcnt(0), other counters untouched
+// s_waitcnt vmcnt(n) with the other counters untouched; n above the counter's
+// 6-bit range is clamped (a wave never has more than 63 operations pending)
+__host__ __device__ constexpr int vm_wait(int n) {
+  return n > 63 ? vm_wait(63) : (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
+}
 
 typedef __attribute__((address_space(3))) void lds_void;
 // 16 bytes per lane from a buffer straight into LDS (lane L at lds + 16 L); kept
@@ -200,18 +206,62 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   const int wu = __builtin_amdgcn_readfirstlane(wid);
   const int lch = (lane & 7) ^ ((4 * (wu & 1) + (lane >> 4)) & 7);
   const int row0 = 8 * wu + (lane >> 3);
-  int va[C::A_CHUNKS];
-#pragma unroll
-  for (int i = 0; i < C::A_CHUNKS; ++i) va[i] = (row0 + 8 * NW * i) * (int)g.lda * 2 + lch * 16;
+  // A stripe i is row0 + 8 NW i: its offset steps by a_step from stripe to
+  // stripe, added in the load sequence itself (an asm add the compiler cannot
+  // hoist) so the loop does not keep A_CHUNKS offsets live in VGPRs
+  const int va0 = row0 * (int)g.lda * 2 + lch * 16;
+  const int a_step = 8 * NW * (int)g.lda * 2;
   const int vb = row0 * (int)g.k * 2 + lch * 16;
 
-  // fragment read offsets: row wm*(BM/WM) + 32i + lr, chunk 2s + lg (swizzle depends on lr only)
-  int ra_off[4], rb_off[4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    ra_off[s] = swz(wm * (BM / WM) + lr, 2 * s + lg);
-    rb_off[s] = swz(wn * (BN / WN) + lr, 2 * s + lg);
+  // fragment read offsets: row wm*(BM/WM) + 32i + lr, chunk 2s + lg; the
+  // swizzle key depends on the row only, so k-step s reads at offset(0) ^ 32 s
+  const int ra0 = swz(wm * (BM / WM) + lr, lg), rb0 = swz(wn * (BN / WN) + lr, lg);
+
+#define WDC_GEMM_LOAD(buf, kt)                                                                     \
+  {                                                                                                \
+    const int kb_ = (kt) * BK * 2;                                                                 \
+    if (wu < NW) {                                                                                 \
+      int v_ = va0;                                                                                \
+      _Pragma("unroll") for (int i = 0; i < C::A_CHUNKS; ++i) {                                     \
+        lds_load16(a_desc, sA + (buf) * BM * 128 + (i * NW + wu) * 1024, v_, kb_);                  \
+        if (i + 1 < C::A_CHUNKS) asm volatile("v_add_u32 %0, %0, %1" : "+v"(v_) : "s"(a_step));     \
+      }                                                                                            \
+      _Pragma("unroll") for (int i = 0; i < C::B_CHUNKS; ++i)                                       \
+          lds_load16(b_desc, sB + (buf) * BN * 128 + (i * NW + wu) * 1024, vb, i * 8 * NW * (int)g.k * 2 + kb_); \
+    }                                                                                              \
   }
+
+  // k-step s of the stage in buffer buf: the wave's TM A and TN B fragments
+#define WDC_GEMM_READ(fa, fb, buf, s)                                                               \
+  {                                                                                                \
+    const char *a_ = sA + (buf) * BM * 128, *b_ = sB + (buf) * BN * 128;                           \
+    const int oa_ = ra0 ^ (32 * (s)), ob_ = rb0 ^ (32 * (s));                                      \
+    _Pragma("unroll") for (int i = 0; i < C::TM; ++i) fa[i] = *(const bf16x8 *)(a_ + oa_ + i * 32 * 128); \
+    _Pragma("unroll") for (int j = 0; j < C::TN; ++j) fb[j] = *(const bf16x8 *)(b_ + ob_ + j * 32 * 128); \
+  }
+  // Workgroup barrier after this wave's LDS reads complete, without the memory
+  // fence of __syncthreads (whose vmcnt(0) would also wait for a stage still
+  // in flight). The wait is the builtin rather than asm so that the compiler's
+  // own wait tracking sees the fragment reads as complete.
+#define WDC_GEMM_BARRIER()                                                                         \
+  {                                                                                                \
+    __builtin_amdgcn_s_waitcnt(WAIT_LGKM0);                                                        \
+    __builtin_amdgcn_s_barrier();                                                                  \
+  }
+
+  constexpr int S = BK / 16;                              // k-steps per stage
+  constexpr int SL = C::A_CHUNKS + C::B_CHUNKS;           // load instructions per loading wave per stage
+  const int nk = (int)(g.k / BK);
+  // Stages 0 and 1 fill both buffers; stage 0 is complete once no more than
+  // stage 1's loads are pending (a wave's memory operations complete in issue
+  // order).
+  WDC_GEMM_LOAD(0, 0);
+  if (nk > 1) WDC_GEMM_LOAD(1, 1);
+  if (wu < NW) {
+    if (nk > 1) __builtin_amdgcn_s_waitcnt(vm_wait(SL));
+    else __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+  }
+  WDC_GEMM_BARRIER();
 
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
@@ -221,65 +271,70 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-#define WDC_GEMM_LOAD(buf, kt)                                                                     \
+  // Software pipeline over two fragment sets x and y: the fragments of k-step
+  // s+1 are read while the MFMAs of step s run. The stage barrier sits before
+  // the last k-step, whose fragments are already in registers: after it the
+  // stage two ahead goes into the buffer just consumed and the next stage's
+  // first fragments are read, both under the last step's MFMAs, so the matrix
+  // cores do not drain at the barrier.
+  static_assert(S == 4, "the x/y alternation assumes four k-steps per stage");
+#define WDC_GEMM_MMA(fa, fb)                                                                       \
   {                                                                                                \
-    const int kb_ = (kt) * BK * 2;                                                                 \
-    if (wu < NW) {                                                                                 \
-      _Pragma("unroll") for (int i = 0; i < C::A_CHUNKS; ++i)                                       \
-          lds_load16(a_desc, sA + (buf) * BM * 128 + (i * NW + wu) * 1024, va[i], kb_);             \
-      _Pragma("unroll") for (int i = 0; i < C::B_CHUNKS; ++i)                                       \
-          lds_load16(b_desc, sB + (buf) * BN * 128 + (i * NW + wu) * 1024, vb, i * 8 * NW * (int)g.k * 2 + kb_); \
-    }                                                                                              \
+    _Pragma("unroll") for (int i = 0; i < C::TM; ++i)                                               \
+    _Pragma("unroll") for (int j = 0; j < C::TN; ++j)                                               \
+        acc[i][j] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0)  \
+                       : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0); \
   }
-
-  const int nk = (int)(g.k / BK);
-  WDC_GEMM_LOAD(0, 0);
-  __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-  __syncthreads();
-
+  bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
+  WDC_GEMM_READ(xa, xb, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) WDC_GEMM_LOAD(buf ^ 1, kt + 1);   // buffer buf^1 was last read in iteration kt-1
-    const char *a = sA + buf * BM * 128, *b = sB + buf * BN * 128;
-#pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      bf16x8 fa[C::TM], fb[C::TN];
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i) fa[i] = *(const bf16x8 *)(a + ra_off[s] + i * 32 * 128);
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) fb[j] = *(const bf16x8 *)(b + rb_off[s] + j * 32 * 128);
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0)
-                         : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-    __syncthreads();
+    WDC_GEMM_READ(ya, yb, buf, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_MMA(xa, xb);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_READ(xa, xb, buf, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_MMA(ya, yb);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_READ(ya, yb, buf, 3);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_MMA(xa, xb);
+    __builtin_amdgcn_sched_barrier(0);
+    // stage kt+1 was requested a stage ago; after the barrier every wave's
+    // reads of buffer buf are complete
+    if (wu < NW) __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+    WDC_GEMM_BARRIER();
+    if (kt + 2 < nk) WDC_GEMM_LOAD(buf, kt + 2);
+    if (kt + 1 < nk) WDC_GEMM_READ(xa, xb, buf ^ 1, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_MMA(ya, yb);
+    __builtin_amdgcn_sched_barrier(0);
   }
-#undef WDC_GEMM_LOAD
+#undef WDC_GEMM_MMA
 
   const bf16_t *bias = (const bf16_t *)g.bias;
   if constexpr (TR) {
     // bf16 output: lane (lr, lg) of tile (i, j) holds row lr of the 32x32 output
     // tile and, in accumulator entries 4q..4q+3, the four consecutive columns
-    // 8q + 4lg + 0..3, stored as one 8-byte group
+    // 8q + 4lg + 0..3, stored as one 8-byte group. The bias of all the lane's
+    // columns is read before the first store, so one wait covers every read.
+    uint2 bw[C::TN][4];
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        bw[j][q] = bias ? *(const uint2 *)(bias + n0 + wn * (BN / WN) + j * 32 + 4 * lg + 8 * q) : make_uint2(0, 0);
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) {
       const int64_t cb = n0 + wn * (BN / WN) + j * 32 + 4 * lg;   // column of group q: cb + 8 q
       float bq[4][4];                                               // bias of the lane's 16 columns
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (bias) {
-          const uint2 bw = *(const uint2 *)(bias + cb + 8 * q);
-          bq[q][0] = bf2f((bf16_t)(bw.x & 0xffff));
-          bq[q][1] = bf2f((bf16_t)(bw.x >> 16));
-          bq[q][2] = bf2f((bf16_t)(bw.y & 0xffff));
-          bq[q][3] = bf2f((bf16_t)(bw.y >> 16));
-        } else {
-          bq[q][0] = bq[q][1] = bq[q][2] = bq[q][3] = 0.f;
-        }
+        bq[q][0] = bf2f((bf16_t)(bw[j][q].x & 0xffff));
+        bq[q][1] = bf2f((bf16_t)(bw[j][q].x >> 16));
+        bq[q][2] = bf2f((bf16_t)(bw[j][q].y & 0xffff));
+        bq[q][3] = bf2f((bf16_t)(bw[j][q].y >> 16));
       }
 #pragma unroll
       for (int i = 0; i < C::TM; ++i) {
@@ -299,11 +354,17 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   } else {
     // float32 output: lane holds column lr of each 32x32 tile, rows
     // 8 (e / 4) + 4 lg + e % 4; 32 lanes cover one 128-byte line per row
+    float bvs[C::TN], gvs[C::TN];
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) {
       const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
-      const float bv = bias ? bf2f(bias[col]) : 0.f;
-      const float gv = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
+      bvs[j] = bias ? bf2f(bias[col]) : 0.f;
+      gvs[j] = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
+      const float bv = bvs[j], gv = gvs[j];
 #pragma unroll
       for (int i = 0; i < C::TM; ++i) {
         const int64_t rb = m0 + wm * (BM / WM) + i * 32 + 4 * lg;   // row of element e: rb + 8 (e / 4) + e % 4
@@ -337,6 +398,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
       }
     }
   }
+#undef WDC_GEMM_READ
+#undef WDC_GEMM_BARRIER
+#undef WDC_GEMM_LOAD
 }
 
 // compute units of the current device (the rectangle order needs exactly 256)
