@@ -276,42 +276,92 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   // the last k-step, whose fragments are already in registers: after it the
   // stage two ahead goes into the buffer just consumed and the next stage's
   // first fragments are read, both under the last step's MFMAs, so the matrix
-  // cores do not drain at the barrier.
+  // cores do not drain at the barrier. Within a step the reads and loads are
+  // interleaved one by one with the MFMAs in a fixed order (a scheduling
+  // barrier after each), so they issue while the wave's MFMAs execute; the
+  // reads go in the order the next step's MFMAs use them (A0, every B, then
+  // the other A fragments).
   static_assert(S == 4, "the x/y alternation assumes four k-steps per stage");
-#define WDC_GEMM_MMA(fa, fb)                                                                       \
+  constexpr int NQ = C::TM * C::TN, NR = C::TM + C::TN;
+#define WDC_GEMM_MFMA1(fa, fb, q)                                                                   \
   {                                                                                                \
-    _Pragma("unroll") for (int i = 0; i < C::TM; ++i)                                               \
-    _Pragma("unroll") for (int j = 0; j < C::TN; ++j)                                               \
-        acc[i][j] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0)  \
-                       : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0); \
+    const int i_ = (q) / C::TN, j_ = (q) % C::TN;                                                  \
+    acc[i_][j_] = TR ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j_], fa[i_], acc[i_][j_], 0, 0, 0) \
+                     : __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i_], fb[j_], acc[i_][j_], 0, 0, 0); \
+  }
+  // read number r of a step: 0 -> A0, 1..TN -> B0..B(TN-1), then A1..A(TM-1)
+#define WDC_GEMM_READ1(fa, fb, buf, s, r)                                                          \
+  {                                                                                                \
+    const bool isb_ = (r) >= 1 && (r) <= C::TN;                                                    \
+    const int ia_ = (r) == 0 ? 0 : (r) - C::TN, jb_ = (r) - 1;                                     \
+    if (isb_)                                                                                      \
+      fb[isb_ ? jb_ : 0] = *(const bf16x8 *)(sB + (buf) * BN * 128 + (rb0 ^ (32 * (s))) + (isb_ ? jb_ : 0) * 32 * 128); \
+    else                                                                                           \
+      fa[isb_ ? 0 : ia_] = *(const bf16x8 *)(sA + (buf) * BM * 128 + (ra0 ^ (32 * (s))) + (isb_ ? 0 : ia_) * 32 * 128); \
+  }
+  // load number l of a stage (A stripes first, then B); v_ steps through the A stripes
+#define WDC_GEMM_LOAD1(buf, kt, l)                                                                 \
+  {                                                                                                \
+    if ((l) < C::A_CHUNKS) {                                                                       \
+      lds_load16(a_desc, sA + (buf) * BM * 128 + ((l) * NW + wu) * 1024, v_, (kt) * BK * 2);       \
+      if ((l) + 1 < C::A_CHUNKS) asm volatile("v_add_u32 %0, %0, %1" : "+v"(v_) : "s"(a_step));     \
+    } else {                                                                                       \
+      const int lb_ = (l) - C::A_CHUNKS;                                                           \
+      lds_load16(b_desc, sB + (buf) * BN * 128 + (lb_ * NW + wu) * 1024, vb,                       \
+                 lb_ * 8 * NW * (int)g.k * 2 + (kt) * BK * 2);                                     \
+    }                                                                                              \
+  }
+  // one k-step: the MFMAs on (ca, cb); if READS, the reads of step rs of buffer
+  // rbuf into (na, nb); if LOADS (a uniform condition), the loads of stage lkt
+  // into buffer lbuf
+#define WDC_GEMM_STEP(ca, cb, na, nb, rbuf, rs, READS, lbuf, lkt, LOADS)                           \
+  {                                                                                                \
+    int v_ = va0;                                                                                  \
+    _Pragma("unroll") for (int q = 0; q < NQ; ++q) {                                               \
+      WDC_GEMM_MFMA1(ca, cb, q);                                                                   \
+      __builtin_amdgcn_sched_barrier(0);                                                           \
+      /* load l goes after MFMA l NQ / SL, read r after MFMA r NQ / NR (constant bounds, */     \
+      /* so the loops unroll fully and every register index is a constant) */                      \
+      /* (LOADS is a run-time condition: the branch holds loads only, so the */                   \
+      /* accumulators never meet at a join) */                                                     \
+      if (LOADS) {                                                                                 \
+        _Pragma("unroll") for (int l = 0; l < SL; ++l) {                                           \
+          if (l * NQ / SL == q) {                                                                  \
+            WDC_GEMM_LOAD1(lbuf, lkt, l);                                                          \
+          }                                                                                        \
+        }                                                                                          \
+      }                                                                                            \
+      __builtin_amdgcn_sched_barrier(0);                                                           \
+      if (READS) {                                                                                 \
+        _Pragma("unroll") for (int r = 0; r < NR; ++r) {                                           \
+          if (r * NQ / NR == q) {                                                                  \
+            WDC_GEMM_READ1(na, nb, rbuf, rs, r);                                                   \
+            __builtin_amdgcn_sched_barrier(0);                                                     \
+          }                                                                                        \
+        }                                                                                          \
+      }                                                                                            \
+    }                                                                                              \
+    (void)v_;                                                                                      \
   }
   bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
   WDC_GEMM_READ(xa, xb, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    WDC_GEMM_READ(ya, yb, buf, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_MMA(xa, xb);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_READ(xa, xb, buf, 2);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_MMA(ya, yb);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_READ(ya, yb, buf, 3);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_MMA(xa, xb);
-    __builtin_amdgcn_sched_barrier(0);
+    WDC_GEMM_STEP(xa, xb, ya, yb, buf, 1, true, 0, 0, false);
+    WDC_GEMM_STEP(ya, yb, xa, xb, buf, 2, true, 0, 0, false);
+    WDC_GEMM_STEP(xa, xb, ya, yb, buf, 3, true, 0, 0, false);
     // stage kt+1 was requested a stage ago; after the barrier every wave's
-    // reads of buffer buf are complete
+    // reads of buffer buf are complete. The last stage's step also reads the
+    // other buffer's first fragments: stale data, never used.
     if (wu < NW) __builtin_amdgcn_s_waitcnt(WAIT_VM0);
     WDC_GEMM_BARRIER();
-    if (kt + 2 < nk) WDC_GEMM_LOAD(buf, kt + 2);
-    if (kt + 1 < nk) WDC_GEMM_READ(xa, xb, buf ^ 1, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    WDC_GEMM_MMA(ya, yb);
-    __builtin_amdgcn_sched_barrier(0);
+    const bool ld = kt + 2 < nk && wu < NW;
+    WDC_GEMM_STEP(ya, yb, xa, xb, buf ^ 1, 0, true, buf, kt + 2, ld);
   }
-#undef WDC_GEMM_MMA
+#undef WDC_GEMM_STEP
+#undef WDC_GEMM_LOAD1
+#undef WDC_GEMM_READ1
+#undef WDC_GEMM_MFMA1
 
   const bf16_t *bias = (const bf16_t *)g.bias;
   if constexpr (TR) {
@@ -463,10 +513,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
       set_lds_limit<128, 128, 2, 2>();
       init = true;
     }
-    // 256 x 256 block tiles: 16 waves of 64 x 64 by default (four per SIMD; 2-6%
-    // faster than 8 waves of 128 x 64 on the N 3072-12288, K 3072 products, even
-    // at K 12288-15360). WDC_GEMM_VARIANT=1 selects 8 waves, 0 four waves of 128 x 128.
-    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 2;
+    // 256 x 256 block tiles: 8 waves of 128 x 64 by default (two per SIMD). With
+    // the reads and loads interleaved into the MFMA stream they are 0.3-1.5%
+    // faster than 16 waves of 64 x 64 on the 13B products and read a quarter
+    // fewer LDS bytes per MFMA (the chip is power-limited under this load).
+    // WDC_GEMM_VARIANT=2 selects 16 waves, 0 four waves of 128 x 128.
+    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
     if (g.n % 256 == 0 && g.m >= 512)
       return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s)
              : variant == 1 ? launch_mfma<256, 256, 2, 4>(g, s)
