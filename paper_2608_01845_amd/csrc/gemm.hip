@@ -125,11 +125,23 @@ __device__ __forceinline__ int swz(int row, int chunk) { return (row * 8 + (chun
 template <int EPI>
 __device__ __forceinline__ float epi_act(float v) {
   if (EPI == EPI_GELU) {
-    // 0.5 v (1 + tanh(u)) = v * sigmoid(2u), u = sqrt(2/pi) (v + 0.044715 v^3)
+    // 0.5 v (1 + tanh(u)) = v * sigmoid(2u), u = sqrt(2/pi) (v + 0.044715 v^3);
+    // the hardware reciprocal (1 ulp) replaces the IEEE division: the result is
+    // rounded to bfloat16 (8 significant bits) anyway
     const float u = 0.7978845608028654f * (v + 0.044715f * v * v * v);
-    return v / (1.f + __expf(-2.f * u));
+    return v * __builtin_amdgcn_rcpf(1.f + __expf(-2.f * u));
   }
   return v;
+}
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+// two floats -> packed bfloat16 pair (one v_cvt_pk_bf16_f32: round to nearest
+// even, NaN stays NaN), low half first
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  bf16x2_t p;
+  p[0] = (__bf16)lo;
+  p[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, p);
 }
 
 template <int BM, int BN, int WM, int WN, int EPI>
@@ -393,10 +405,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
         bf16_t *out = (bf16_t *)g.c + row * g.ldc + cb;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const uint32_t w0 = (uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 0] + bq[q][0])) |
-                              ((uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 1] + bq[q][1])) << 16);
-          const uint32_t w1 = (uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 2] + bq[q][2])) |
-                              ((uint32_t)f2bf(epi_act<EPI>(acc[i][j][4 * q + 3] + bq[q][3])) << 16);
+          const uint32_t w0 = pack_bf16(epi_act<EPI>(acc[i][j][4 * q + 0] + bq[q][0]),
+                                        epi_act<EPI>(acc[i][j][4 * q + 1] + bq[q][1]));
+          const uint32_t w1 = pack_bf16(epi_act<EPI>(acc[i][j][4 * q + 2] + bq[q][2]),
+                                        epi_act<EPI>(acc[i][j][4 * q + 3] + bq[q][3]));
           *(uint2 *)(out + 8 * q) = make_uint2(w0, w1);
         }
       }
