@@ -531,10 +531,39 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
     // fewer LDS bytes per MFMA (the chip is power-limited under this load).
     // WDC_GEMM_VARIANT=2 selects 16 waves, 0 four waves of 128 x 128.
     static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
-    if (g.n % 256 == 0 && g.m >= 512)
-      return variant == 0 ? launch_mfma<256, 256, 2, 2>(g, s)
-             : variant == 1 ? launch_mfma<256, 256, 2, 4>(g, s)
-                            : launch_mfma<256, 256, 4, 4>(g, s);
+    auto big = [&](const GemmArgs &gg) {
+      return variant == 0 ? launch_mfma<256, 256, 2, 2>(gg, s)
+             : variant == 1 ? launch_mfma<256, 256, 2, 4>(gg, s)
+                            : launch_mfma<256, 256, 4, 4>(gg, s);
+    };
+    if (g.n % 256 == 0 && g.m >= 512) {
+      // Tail split for a single large long-K product on a 256-CU device: the
+      // rows whose 256 x 256 tiles fill whole dispatch rounds (m1 tiles, a
+      // multiple of 256 / gcd(n_tiles, 256)) run as above; the remaining rows,
+      // which would leave most CUs idle in a last round at most half full, run
+      // as 128 x 128 tiles (two blocks per CU). At M = 67,576 and N = 3,072 that
+      // turns 12.375 rounds into 12 plus 2,040 rows: +1.5% at K = 12,288, +2% at
+      // K = 15,360; at K = 3,072 the small tiles' lower efficiency costs more
+      // than the idle CUs (-1.3%), so short products keep one launch.
+      static const int split = getenv("WDC_GEMM_SPLIT") ? atoi(getenv("WDC_GEMM_SPLIT")) : 1;
+      const int64_t m_tiles = (g.m + 255) / 256, n_tiles = g.n / 256;
+      int64_t gcd = n_tiles, r = 256;
+      while (r) { const int64_t t = gcd % r; gcd = r; r = t; }
+      const int64_t m1 = m_tiles / (256 / gcd) * (256 / gcd) * 256;   // rows in whole rounds
+      const bool thin_tail = (m_tiles * n_tiles) % 256 != 0 && (m_tiles * n_tiles) % 256 <= 128;
+      if (split && g.batch <= 1 && g.k >= 8192 && thin_tail && device_cus() == 256 && m1 > 0 && m1 < g.m) {
+        GemmArgs g1 = g, g2 = g;
+        g1.m = m1;
+        g2.m = g.m - m1;
+        g2.a = (const bf16_t *)g.a + m1 * g.lda;
+        const bool c16 = g.epi == EPI_STORE || g.epi == EPI_GELU;
+        g2.c = c16 ? (void *)((bf16_t *)g.c + m1 * g.ldc) : (void *)((float *)g.c + m1 * g.ldc);
+        hipError_t e = big(g1);
+        if (e != hipSuccess) return e;
+        return launch_mfma<128, 128, 2, 2>(g2, s);
+      }
+      return big(g);
+    }
     if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
   }
   dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64), g.batch > 1 ? g.batch : 1), block(256);

@@ -72,6 +72,30 @@ def test_linear_large_product_rectangle_order():
     assert err <= 4e-3, err
 
 
+def test_linear_long_k_tail_split():
+    """A long-K product whose last dispatch round would be thin (9 M tiles x 32
+    N tiles = 288 tiles, 32 past the last whole round of 256): the first 2,048
+    rows run as 256 x 256 tiles and the last 100 as 128 x 128 tiles (a second
+    launch). Sampled rows of the first part and every row of the second against
+    the oracle."""
+    torch = torch_cuda()
+    cfg = synth.get_config("mid")
+    ctx = context(cfg, weights=False)
+    m, n, k = 2148, 8192, 8192
+    rng = _rng(2025)
+    a = synth.stored(rng.standard_normal((m, k), dtype=np.float32), cfg.dtype)
+    w = synth.stored(rng.standard_normal((n, k), dtype=np.float32) * 0.02, cfg.dtype)
+    b = synth.stored(rng.standard_normal(n, dtype=np.float32) * 0.1, cfg.dtype)
+    out = torch.empty((m, n), dtype=ctx.tdtype, device="cuda")
+    ctx.linear(ctx.to_device(a), ctx.to_device(w), ctx.to_device(b), out, m, n, k)
+    rows = np.unique(np.concatenate([rng.choice(2048, 48, replace=False), np.arange(2040, m)]))
+    got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    ref = dit.linear({"l.w": w, "l.b": b}, "l", a[rows].astype(np.float64))
+    err = rel_l2(got, ref)
+    print("rows", len(rows), "rel_l2", err)
+    assert err <= 4e-3, err
+
+
 def _attn_inputs(ctx, heads, hd, n, seed, bf16):
     rng = _rng(seed)
     q, k, v = (rng.standard_normal((heads, n, hd)) for _ in range(3))
