@@ -126,10 +126,11 @@ template <int EPI>
 __device__ __forceinline__ float epi_act(float v) {
   if (EPI == EPI_GELU) {
     // 0.5 v (1 + tanh(u)) = v * sigmoid(2u), u = sqrt(2/pi) (v + 0.044715 v^3);
-    // the hardware reciprocal (1 ulp) replaces the IEEE division: the result is
-    // rounded to bfloat16 (8 significant bits) anyway
-    const float u = 0.7978845608028654f * (v + 0.044715f * v * v * v);
-    return v * __builtin_amdgcn_rcpf(1.f + __expf(-2.f * u));
+    // the hardware exp2 and reciprocal (about 1 ulp each) replace exp and the
+    // IEEE division: the result is rounded to bfloat16 (8 significant bits)
+    // exp(-2u) = exp2(v (A + B v^2)), A = -2 sqrt(2/pi) log2(e), B = 0.044715 A
+    constexpr float A = -2.f * 0.7978845608028654f * 1.4426950408889634f, B = 0.044715f * A;
+    return v * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(v * fmaf(B, v * v, A)));
   }
   return v;
 }
