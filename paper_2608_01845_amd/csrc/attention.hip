@@ -12,8 +12,11 @@
 //    8 accumulator values a lane holds for 16 consecutive keys become its 8
 //    bf16 k-values, and the V^T operand is read with the same key order, so P
 //    never goes through LDS;
-//  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr, the
-//    default), or with a running max (k_attn_bf16_pp, kept for comparison).
+//  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr3, the
+//    default at hd 128, whose step runs the vector work of tile t + 1 inside
+//    the MFMA stream of tiles t and t + 2; k_attn_bf16_ppr, the two-phase form
+//    and the default at hd 64), or with a running max (k_attn_bf16_pp, kept
+//    for comparison).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
@@ -639,6 +642,263 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   }
 }
 
+// Three-stage form of the reference-max kernel: step t runs the P V MFMAs of
+// tile t and the Q K MFMAs of tile t + 2 with the vector phase of tile t + 1
+// (P = exp2(S'), its bf16 conversion and row sum) interleaved into the same
+// instruction stream, so a wave's VALU work executes under its own MFMAs
+// instead of in a separate phase that the two waves of a SIMD run together.
+// S and P are double-buffered (S of t + 1 and t + 2, P of t and t + 1). Tile j
+// sits in slot j % 4: step t reads K_{t+2} and V_t, loads K_{t+4} into the
+// slot of K_t (last read in step t - 2, or by the prologue for t = 0, hence
+// one more barrier there) and V_{t+2} into the slot of V_{t-2} (last read in
+// step t - 2).
+template <int HD>
+__global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
+  constexpr int QB = 256;                  // 8 waves x 32 queries
+  constexpr int NB = 4;                    // K buffers and V^T buffers
+  constexpr int K_BYTES = KV * HD * 2;
+  constexpr int V_BASE = NB * K_BYTES;     // V^T buffers follow the K buffers
+  using TL = TileLoad<HD>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+
+  int h = blockIdx.y, qb = blockIdx.x;
+  if (a.xcd_order) {
+    const int id = blockIdx.x + blockIdx.y * gridDim.x;
+    const int li = id >> 3;
+    h = (id & 7) + 8 * (li / gridDim.x);
+    qb = li % gridDim.x;
+  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool grp_a = wid < 4;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int64_t qbase = (int64_t)qb * QB + wid * 32;
+  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
+
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+  bf16x8 qf[HD / 16];                      // Q^T scaled by sc: scores in log2 units
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) {
+    const bf16x8 raw = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) qf[s][j] = (__bf16)((float)raw[j] * sc);
+  }
+
+  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+  const int lw = wid & 3;
+  const TileLoad<HD> tl(lw, lane, a.n_pad);
+  int kro[HD / 16];
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
+  int vro[4];                              // V^T fragment offsets, V region base folded in
+#pragma unroll
+  for (int j = 0; j < 4; ++j) vro[j] = V_BASE + vslot(lr, 2 * j + lg);
+
+  const int ntiles = (int)((a.n + KV - 1) / KV);
+  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
+  auto load_k = [&](int b, int tile) {
+#pragma unroll
+    for (int i = 0; i < TL::K_STRIPES; ++i)
+      lds_load16(kdesc, smem + b * K_BYTES + lw * 1024 + i * 4096, tl.kvo, tile * KV * HD * 2 + i * 4096);
+  };
+  auto load_v = [&](int b, int tile) {
+#pragma unroll
+    for (int i = 0; i < TL::V_STRIPES; ++i)
+      lds_load16(vdesc, smem + V_BASE + b * K_BYTES + lw * 1024 + i * 4096, tl.vvo,
+                 tile * KV * 2 + i * 32 * (int)a.n_pad * 2);
+  };
+
+  if (grp_a) {                             // K_0..K_3, V_0, V_1
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (j < ntiles) load_k(j, j);
+    load_v(0, 0);
+    if (ntiles > 1) load_v(1, 1);
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+  }
+  __syncthreads();
+
+  f32x16 o[HD / 32];
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
+  bf16x8 ones;                             // key-side partner of the -m fragment
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones[j] = (__bf16)0.f;
+  if (lg == 0) {
+    ones[0] = (__bf16)1.f;
+    ones[1] = (__bf16)1.f;
+  }
+  float m = 0.f, l = 0.f;
+  bf16x8 mf = ppr_mfrag(m, lg);
+  f32x16 S[2][2];                          // S' of tiles t + 1 and t + 2 (index tile & 1)
+  bf16x8 pf[2][4];                         // P of tiles t and t + 1 (index tile & 1)
+  ppr_qk<HD>(S[0], smem, qf, kro, ones, mf);
+  {                                        // m = the first tile's row max
+    const int v0 = ntiles == 1 ? last_valid : KV;
+    if (v0 < KV) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= v0) S[0][kt][e] = -1e30f;
+    }
+    m = ppr_rowmax(S[0]);
+    mf = ppr_mfrag(m, lg);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S[0][kt][e] -= m;
+    l = ppr_exp(S[0], pf[0]);
+  }
+  if (ntiles > 1) ppr_qk<HD>(S[1], smem + K_BYTES, qf, kro, ones, mf);
+  // step 0 refills the slot of K_0, which every wave has just read
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per step
+  static_assert(NMF == 32, "the fixed-order step assumes 16 P V and 16 Q K reads (hd 128)");
+  const bf16x2_t one2_ = {(__bf16)1.f, (__bf16)1.f};
+  // fragment read r of a step: 0-15 V^T (k-step r / (HD/32), O tile r % (HD/32)),
+  // 16-31 K (hd step (r-16) / 2, key half (r-16) % 2)
+#define WDC_PPR3_READ(r)                                                                         \
+  {                                                                                              \
+    if ((r) < 16)                                                                                \
+      fr_[(r)] = *(const bf16x8 *)(vb_ + ((r) % (HD / 32)) * 32 * KV * 2 + vro[(r) / (HD / 32)]); \
+    else                                                                                         \
+      fr_[(r)] = *(const bf16x8 *)(kb_ + kro[((r) >= 16 ? (r) - 16 : 0) / 2] + (((r) - 16) % 2) * 32 * HD * 2); \
+  }
+  // One tile step with compile-time slot P = t % NB; c = (t + 1) & 1 indexes
+  // S' of tile t + 1 and the P it becomes, n = t & 1 the S' of tile t + 2 and
+  // the P of tile t.
+#define WDC_PPR3_STEP(P)                                                                         \
+  {                                                                                              \
+    constexpr int c = ((P) + 1) & 1, n = (P) & 1;                                                \
+    const int t = t0 + (P);                                                                      \
+    int issued = 0;                                                                              \
+    if (grp_a) {                                                                                 \
+      if (t + 4 < ntiles) {                                                                      \
+        load_k((P), t + 4);                                                                      \
+        issued += TL::K_STRIPES;                                                                 \
+      }                                                                                          \
+      if (t + 2 < ntiles) {                                                                      \
+        load_v(((P) + 2) % NB, t + 2);                                                           \
+        issued += TL::V_STRIPES;                                                                 \
+      }                                                                                          \
+    }                                                                                            \
+    const bool soft = t + 1 < ntiles;                                                            \
+    if (t + 2 == ntiles && last_valid < KV) {  /* tile t + 1 is the partial last one */         \
+      asm volatile("" ::: "memory");                                                             \
+      _Pragma("unroll") for (int kt = 0; kt < 2; ++kt)                                           \
+      _Pragma("unroll") for (int e = 0; e < 16; ++e)                                             \
+        if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= last_valid) S[c][kt][e] = -1e30f;        \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    /* One fixed-order stream (unconditional: past the end the Q K reads a stale */              \
+    /* K slot and the exponentials a stale S', and neither result is used). MFMA */               \
+    /* q: 0-15 P V (k-step j = q / (HD/32), O tile i = q % (HD/32)), 16-17 the -m */             \
+    /* seeds, 18-33 Q K (hd step (q-18) / 2, key half (q-18) % 2); fragment read r */             \
+    /* (r = q for P V, q - 2 for Q K) goes out four reads ahead of its MFMA; after */             \
+    /* MFMA q < 32 comes exponential q of S'_{t+1}, after every second one the */                 \
+    /* bf16 pair and its row-sum dot product. */                                                  \
+    const char *vb_ = smem + (P) * K_BYTES, *kb_ = smem + (((P) + 2) % NB) * K_BYTES;             \
+    bf16x8 fr_[NMF];                                                                             \
+    float ls = 0.f;                                                                              \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) WDC_PPR3_READ(r_);                          \
+    _Pragma("unroll") for (int q_ = 0; q_ < 34; ++q_) {                                          \
+      if (q_ < 16) {                                                                             \
+        constexpr int NI = HD / 32;                                                              \
+        o[q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_ < 16 ? q_ : 0], pf[n][q_ / NI], o[q_ % NI], 0, 0, 0); \
+      } else if (q_ < 18) {                                                                      \
+        f32x16 z_;                                                                               \
+        _Pragma("unroll") for (int e = 0; e < 16; ++e) z_[e] = 0.f;                              \
+        S[n][q_ - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, z_, 0, 0, 0);          \
+      } else {                                                                                   \
+        const int r_ = q_ - 2;                                                                   \
+        S[n][(r_ - 16) % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[r_ >= 16 ? r_ : 16], qf[(r_ - 16) / 2], S[n][(r_ - 16) % 2], 0, 0, 0); \
+      }                                                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      if (q_ < 16 || q_ >= 18) {                                                                 \
+        const int r_ = q_ < 16 ? q_ : q_ - 2;                                                    \
+        if (r_ + 4 < NMF) WDC_PPR3_READ(r_ + 4);                                                 \
+      }                                                                                          \
+      if (q_ < 32) {                                                                             \
+        const int kt_ = q_ / 16, e_ = q_ % 16;                                                   \
+        pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);        \
+        if (q_ & 1)                                                                              \
+          ls = __builtin_amdgcn_fdot2_f32_bf16(                                                  \
+              bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false); \
+      }                                                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+    }                                                                                            \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    if (soft) {                                                                                  \
+      if (__any(ls > PPR_LIMIT)) {                                                               \
+        const float mx = ppr_rowmax(S[c]);                                                       \
+        float mn = m + (mx > 8.f ? mx : 0.f);                                                    \
+        mf = ppr_mfrag(mn, lg);                                                                  \
+        const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);                              \
+        m = mn;                                                                                  \
+        l *= alpha;                                                                              \
+        _Pragma("unroll") for (int i = 0; i < HD / 32; ++i)                                      \
+        _Pragma("unroll") for (int e = 0; e < 16; ++e) o[i][e] *= alpha;                         \
+        _Pragma("unroll") for (int kt = 0; kt < 2; ++kt)                                         \
+        _Pragma("unroll") for (int e = 0; e < 16; ++e) {                                         \
+          S[c][kt][e] -= d;                                                                      \
+          S[n][kt][e] -= d;                                                                      \
+        }                                                                                        \
+        ls = ppr_exp(S[c], pf[c]);                                                               \
+      }                                                                                          \
+      l += ls;                                                                                   \
+    }                                                                                            \
+    if (grp_a) pp_wait4<HD>(issued);                                                             \
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
+  }
+  for (int t0 = 0; t0 < ntiles; t0 += NB) {
+    WDC_PPR3_STEP(0)
+    if (t0 + 1 >= ntiles) break;
+    WDC_PPR3_STEP(1)
+    if (t0 + 2 >= ntiles) break;
+    WDC_PPR3_STEP(2)
+    if (t0 + 3 >= ntiles) break;
+    WDC_PPR3_STEP(3)
+  }
+#undef WDC_PPR3_STEP
+#undef WDC_PPR3_READ
+
+  const float lt = l + __shfl_xor(l, 32, 64);
+  const float inv = 1.f / lt;
+  const int64_t q = qbase + lr;
+  if (q < a.n) {
+    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
+#pragma unroll
+    for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = 32 * i + 8 * g4 + 4 * lg;
+        uint32_t w0 = (uint32_t)f2bf(o[i][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 1] * inv) << 16);
+        uint32_t w1 = (uint32_t)f2bf(o[i][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 3] * inv) << 16);
+        *(uint2 *)(O + d0) = make_uint2(w0, w1);
+      }
+  }
+}
+
+template <int HD>
+hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
+  constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
+  static bool init = false;
+  if (!init) {
+    hipFuncSetAttribute((const void *)k_attn_bf16_ppr3<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    init = true;
+  }
+  dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
+  hipLaunchKernelGGL((k_attn_bf16_ppr3<HD>), grid, dim3(512), LDS, s, a);
+  return hipGetLastError();
+}
+
 template <int HD>
 hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
   constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
@@ -673,13 +933,17 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
     // Default: the 8-wave reference-max kernel with four-deep tile buffers and
-    // one barrier per tile (ppr). WDC_ATTN_VARIANT=3 selects the earlier
-    // ping-pong form (3 K / 2 V buffers, running-max softmax) for comparison.
-    static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 4;
+    // one barrier per tile, in its three-stage form at hd 128 (ppr3: 3.5-4.5%
+    // faster than the two-phase ppr at the 13B shape) and its two-phase form at
+    // hd 64 (the fixed-order stream is written for hd 128).
+    // WDC_ATTN_VARIANT=4 selects ppr at hd 128 too, 3 the earlier ping-pong form
+    // (3 K / 2 V buffers, running-max softmax), for comparison.
+    static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 5;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
     b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
-    if (a.hd == 128) return variant == 3 ? launch_bf16_pp<128>(b, s) : launch_bf16_ppr<128>(b, s);
+    if (a.hd == 128)
+      return variant == 3 ? launch_bf16_pp<128>(b, s) : variant == 4 ? launch_bf16_ppr<128>(b, s) : launch_bf16_ppr3<128>(b, s);
     if (a.hd == 64) return variant == 3 ? launch_bf16_pp<64>(b, s) : launch_bf16_ppr<64>(b, s);
     return hipErrorInvalidValue;
   }
