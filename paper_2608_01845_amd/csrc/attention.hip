@@ -15,8 +15,7 @@
 //  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr3, the
 //    default at hd 128, whose step runs the vector work of tile t + 1 inside
 //    the MFMA stream of tiles t and t + 2; k_attn_bf16_ppr, the two-phase form
-//    and the default at hd 64), or with a running max (k_attn_bf16_pp, kept
-//    for comparison).
+//    and the default at hd 64).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
@@ -144,33 +143,8 @@ struct TileLoad {
   }
 };
 
-// Ping-pong variant: 8 wavefronts per block in two groups of 4 (waves w and
-// w + 4 share a SIMD). Every tile step has an MFMA phase (O += V^T P^T for tile
-// t, S = K Q^T for tile t+1) and a vector phase (online softmax of S), each
-// closed by a block barrier; group B starts one barrier late, so on every SIMD
-// one wave's softmax runs while the other wave's matrix work does.
-// Group A issues the direct LDS loads of K_{t+2} and V_{t+1} at the start of
-// its MFMA phase of tile t and waits for them before the barrier that closes
-// its vector phase. K is triple-buffered (tile t in kbuf[t % 3]) and V double-
-// buffered: the buffers written in step t held K_{t-1} and V_{t-1}, whose last
-// readers (group B's matrix phase of step t-2 for K, t-1 for V) finished at
-// least one barrier before the loads are issued.
-template <int HD>
-__device__ __forceinline__ void pp_qk(f32x16 (&S)[2], const char *k, const bf16x8 (&qf)[HD / 16],
-                                      const int (&kro)[HD / 16]) {
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) S[kt][e] = 0.f;
-#pragma unroll
-  for (int st_ = 0; st_ < HD / 16; ++st_)
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      const bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
-      S[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st_], S[kt], 0, 0, 0);
-    }
-}
-
+// O^T += V^T P^T for one tile: the V^T fragment (O tile i, k-step j) is read
+// right before its MFMA.
 template <int HD>
 __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const bf16x8 (&pf)[4],
                                       const int (&vro)[4]) {
@@ -183,171 +157,7 @@ __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const
     }
 }
 
-// softmax of S (keys >= valid masked) -> bf16 P; rescales O and l when the max moves
-template <int HD>
-__device__ __forceinline__ void pp_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32x16 (&o)[HD / 32], float &m,
-                                           float &l, float sc, int valid, int lg) {
-  if (valid < KV) {
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= valid) S[kt][e] = -1e30f;
-  }
-  float mx = S[0][0];
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, S[kt][e]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  const float mn = fmaxf(m, mx * sc);
-  if (__any(mn > m)) {
-    const float alpha = __builtin_amdgcn_exp2f(m - mn);
-    l *= alpha;
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
-  }
-  m = mn;
-  float sum = 0.f;
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float p = __builtin_amdgcn_exp2f(fmaf(S[kt][e], sc, -mn));
-      sum += p;
-      pf[2 * kt + e / 8][e % 8] = (__bf16)p;
-    }
-  l += sum;
-}
-
-template <int HD>
-__global__ __launch_bounds__(512, 1) void k_attn_bf16_pp(AttnArgs a) {
-  constexpr int QB = 256;                  // 8 waves x 32 queries
-  constexpr int K_BYTES = KV * HD * 2;
-  using TL = TileLoad<HD>;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-  char *sK = smem;                         // [3][KV][HD]
-  char *sV = smem + 3 * K_BYTES;           // [2][HD][KV]
-
-  int h = blockIdx.y, qb = blockIdx.x;
-  if (a.xcd_order) {
-    const int id = blockIdx.x + blockIdx.y * gridDim.x;
-    const int li = id >> 3;
-    h = (id & 7) + 8 * (li / gridDim.x);
-    qb = li % gridDim.x;
-  }
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool grp_a = wid < 4;
-  const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qbase = (int64_t)qb * QB + wid * 32;
-  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
-
-  bf16x8 qf[HD / 16];
-#pragma unroll
-  for (int s = 0; s < HD / 16; ++s) qf[s] = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
-
-  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const int lw = wid & 3;                  // loader index inside group A
-  const TileLoad<HD> tl(lw, lane, a.n_pad);
-  int kro[HD / 16];
-#pragma unroll
-  for (int s = 0; s < HD / 16; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) vro[j] = vslot(lr, 2 * j + lg);
-
-  const int ntiles = (int)((a.n + KV - 1) / KV);
-  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
-  auto load_k = [&](int b, int tile) {
-#pragma unroll
-    for (int i = 0; i < TL::K_STRIPES; ++i)
-      lds_load16(kdesc, sK + b * K_BYTES + lw * 1024 + i * 4096, tl.kvo, tile * KV * HD * 2 + i * 4096);
-  };
-  auto load_v = [&](int b, int tile) {
-#pragma unroll
-    for (int i = 0; i < TL::V_STRIPES; ++i)
-      lds_load16(vdesc, sV + b * K_BYTES + lw * 1024 + i * 4096, tl.vvo, tile * KV * 2 + i * 32 * (int)a.n_pad * 2);
-  };
-
-  if (grp_a) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (ntiles > 1) load_k(1, 1);
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-  }
-  __syncthreads();
-
-  f32x16 o[HD / 32];
-#pragma unroll
-  for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  float m = -1e30f, l = 0.f;
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
-  f32x16 S[2];
-  bf16x8 pf[4];
-  pp_qk<HD>(S, sK, qf, kro);
-  pp_softmax<HD>(S, pf, o, m, l, sc, ntiles == 1 ? last_valid : KV, lg);
-  if (!grp_a) __syncthreads();             // group B runs one phase behind
-
-  for (int t = 0; t < ntiles; ++t) {
-    const bool more = t + 1 < ntiles;
-    // matrix phase
-    if (grp_a) {
-      if (t + 2 < ntiles) load_k((t + 2) % 3, t + 2);
-      if (more) load_v((t + 1) & 1, t + 1);
-    }
-    // Matrix work of the phase as one scheduling region: O += V^T P^T, then
-    // S = K Q^T for the next tile (on the last tile it reads a stale buffer and
-    // S goes unused). LDS fragment reads are kept four ahead of the MFMAs.
-    __builtin_amdgcn_sched_barrier(0);
-    pp_pv<HD>(o, sV + (t & 1) * K_BYTES, pf, vro);
-    pp_qk<HD>(S, sK + ((t + 1) % 3) * K_BYTES, qf, kro);
-    constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);     // MFMAs = fragment reads in the region
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int i = 0; i < NMF - 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    // Barrier that waits only for this wave's LDS reads (the buffers refilled
-    // next must be free), not for group A's tile loads still in flight: those
-    // are waited for before the barrier that closes the vector phase, which is
-    // the first point any wave reads them.
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    // vector phase
-    if (more) pp_softmax<HD>(S, pf, o, m, l, sc, t + 2 < ntiles ? KV : last_valid, lg);
-    if (grp_a) __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-    __syncthreads();
-  }
-  if (grp_a) __syncthreads();              // match group B's extra barrier
-
-  const float lt = l + __shfl_xor(l, 32, 64);
-  const float inv = 1.f / lt;
-  const int64_t q = qbase + lr;
-  if (q < a.n) {
-    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * i + 8 * g4 + 4 * lg;
-        uint32_t w0 = (uint32_t)f2bf(o[i][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 1] * inv) << 16);
-        uint32_t w1 = (uint32_t)f2bf(o[i][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 3] * inv) << 16);
-        *(uint2 *)(O + d0) = make_uint2(w0, w1);
-      }
-  }
-}
-
-// Reference-max kernel (ppr), the default form. 8 wavefronts per block (two
+// Reference-max kernel (ppr), the two-phase form. 8 wavefronts per block (two
 // per SIMD), 32 queries each, K/V tiles of 64 keys in four K and four V^T LDS
 // buffers. Every tile step of a wave is a matrix phase (O += V^T P^T for tile t,
 // S' for tile t+1, LDS fragment reads scheduled four ahead of the MFMAs)
@@ -913,18 +723,6 @@ hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
 }
 
 
-template <int HD>
-hipError_t launch_bf16_pp(const AttnArgs &a, hipStream_t s) {
-  constexpr int LDS = (3 + 2) * KV * HD * 2;   // three K tiles, two V^T tiles
-  static bool init = false;
-  if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16_pp<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
-    init = true;
-  }
-  dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16_pp<HD>), grid, dim3(512), LDS, s, a);
-  return hipGetLastError();
-}
 
 }  // namespace
 
@@ -936,15 +734,14 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
     // one barrier per tile, in its three-stage form at hd 128 (ppr3: 3.5-4.5%
     // faster than the two-phase ppr at the 13B shape) and its two-phase form at
     // hd 64 (the fixed-order stream is written for hd 128).
-    // WDC_ATTN_VARIANT=4 selects ppr at hd 128 too, 3 the earlier ping-pong form
-    // (3 K / 2 V buffers, running-max softmax), for comparison.
+    // WDC_ATTN_VARIANT=4 selects ppr at hd 128 too, for comparison.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 5;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
     b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
     if (a.hd == 128)
-      return variant == 3 ? launch_bf16_pp<128>(b, s) : variant == 4 ? launch_bf16_ppr<128>(b, s) : launch_bf16_ppr3<128>(b, s);
-    if (a.hd == 64) return variant == 3 ? launch_bf16_pp<64>(b, s) : launch_bf16_ppr<64>(b, s);
+      return variant == 4 ? launch_bf16_ppr<128>(b, s) : launch_bf16_ppr3<128>(b, s);
+    if (a.hd == 64) return launch_bf16_ppr<64>(b, s);
     return hipErrorInvalidValue;
   }
   dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);
