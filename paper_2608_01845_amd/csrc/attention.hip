@@ -699,10 +699,10 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
 template <int HD>
 hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
   constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
-  static bool init = false;
-  if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16_ppr3<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
-    init = true;
+  static bool seen[64] = {};
+  if (first_on_device(seen)) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_attn_bf16_ppr3<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    if (e != hipSuccess) return e;
   }
   dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
   hipLaunchKernelGGL((k_attn_bf16_ppr3<HD>), grid, dim3(512), LDS, s, a);
@@ -712,10 +712,10 @@ hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
 template <int HD>
 hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
   constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
-  static bool init = false;
-  if (!init) {
-    hipFuncSetAttribute((const void *)k_attn_bf16_ppr<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
-    init = true;
+  static bool seen[64] = {};
+  if (first_on_device(seen)) {
+    const hipError_t e = hipFuncSetAttribute((const void *)k_attn_bf16_ppr<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+    if (e != hipSuccess) return e;
   }
   dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
   hipLaunchKernelGGL((k_attn_bf16_ppr<HD>), grid, dim3(512), LDS, s, a);

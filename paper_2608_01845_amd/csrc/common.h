@@ -109,6 +109,17 @@ struct GemmArgs {
 // dtype: 0 float32, 1 bfloat16
 hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s);
 
+// True the first time it is called with this flag array on the current device
+// (kernel attributes such as the dynamic LDS limit are set per device). A
+// device id outside the array, or a failed query, always answers true.
+inline bool first_on_device(bool (&seen)[64]) {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess || d < 0 || d >= 64) return true;
+  if (seen[d]) return false;
+  seen[d] = true;
+  return true;
+}
+
 // ------------------------------------------------------------------ attention
 struct AttnArgs {
   const void *q, *k, *v;  // see wdc_attention

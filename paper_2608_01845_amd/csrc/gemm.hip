@@ -502,12 +502,17 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
 }
 
 template <int BM, int BN, int WM, int WN>
-void set_lds_limit() {
+hipError_t set_lds_limit() {
   using C = Cfg<BM, BN, WM, WN>;
-  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-  hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+  const void *k[4] = {(const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>,
+                      (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>,
+                      (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>,
+                      (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>};
+  for (const void *f : k) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 }  // namespace
 
@@ -518,13 +523,13 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
                        (uintptr_t)g.c % 16 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.bias % 8 == 0 &&
                        (uintptr_t)g.gate % 16 == 0 && (g.batch <= 1 || (g.a_bs % 8 == 0 && g.c_bs % 4 == 0 && g.gate_bs % 4 == 0));
   if (dtype == 1 && aligned) {
-    static bool init = false;
-    if (!init) {
-      set_lds_limit<256, 256, 2, 2>();
-      set_lds_limit<256, 256, 2, 4>();
-      set_lds_limit<256, 256, 4, 4>();
-      set_lds_limit<128, 128, 2, 2>();
-      init = true;
+    static bool seen[64] = {};
+    if (first_on_device(seen)) {
+      hipError_t e = set_lds_limit<256, 256, 2, 2>();
+      if (e == hipSuccess) e = set_lds_limit<256, 256, 2, 4>();
+      if (e == hipSuccess) e = set_lds_limit<256, 256, 4, 4>();
+      if (e == hipSuccess) e = set_lds_limit<128, 128, 2, 2>();
+      if (e != hipSuccess) return e;
     }
     // 256 x 256 block tiles: 8 waves of 128 x 64 by default (two per SIMD). With
     // the reads and loads interleaved into the MFMA stream they are 0.3-1.5%
