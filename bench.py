@@ -32,7 +32,7 @@ PEAK_HBM_GBS = 8000.0
 # copy; profiles/attention_13b_hbm_traffic.md). Valid only for the kernel
 # version named here; set to None whenever that kernel changes.
 MEASURED_TRAFFIC = {"k_attn_bf16_ppr3<128>": 8.305e9}
-ATTN_KERNEL = "k_attn_bf16_ppr3<128>"
+ATTN_KERNEL = {128: "k_attn_bf16_ppr3<128>", 64: "k_attn_bf16_ppr<64>"}   # default bf16 kernel by head size
 METRIC = "DiT fwd TFLOP/s (% bf16 MFMA peak) + denoising steps/s at 13B shape"
 
 
@@ -329,11 +329,11 @@ def main():
                     "gemm_ms_total": round(gemm_ms, 1), "gemm_launches": gemm_n,
                     "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None,
                     "layernorm_modulate": hbm_entry(norm_ms, norm_n, norm_work)},
-        "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL,
+        "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL.get(cfg.head_dim),
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
-                     "traffic": MEASURED_TRAFFIC.get(ATTN_KERNEL) if args.workload == "13b" else None,
+                     "traffic": MEASURED_TRAFFIC.get(ATTN_KERNEL.get(cfg.head_dim)) if args.workload == "13b" else None,
                      "traffic_unit": "bytes per launch"},
     }
     if args.rollout:
