@@ -3,10 +3,15 @@
 // float32 store). Both operands are K-contiguous ("NT"), which is the layout
 // the MFMA operand registers want: every lane loads 8 consecutive bf16.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 tiles, BMxBN block tile, BK = 64,
-// double-buffered LDS with an XOR swizzle of the 16-byte chunks of each
-// 128-byte row (conflict-free fragment reads), the next K tile loaded straight
-// from HBM into the other LDS buffer while the current one feeds the matrix cores.
+// bf16 path: v_mfma_f32_32x32x16_bf16 tiles, BMxBN block tile (256 x 256 in 8
+// waves of 128 x 64 for the large products), BK = 64, double-buffered LDS with
+// an XOR swizzle of the 16-byte chunks of each 128-byte row (conflict-free
+// fragment reads). K stages go straight from HBM into LDS (buffer loads with the
+// LDS flag) two stages ahead; each wave reads its fragments one k-step ahead,
+// one read at a time between its MFMAs, and the stage barrier sits before a
+// stage's last k-step so the matrix cores never drain at it. Large single
+// products take an XCD-aware block order, and long-K ones whose last dispatch
+// round would be thin run their last rows as a second launch of 128 x 128 tiles.
 // float32 path (tiny fp32 workload, and shapes the MFMA tiles do not cover):
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
