@@ -85,7 +85,10 @@ enum Epi {
   EPI_STORE = 0,     // c = acc + bias (model dtype)
   EPI_GELU = 1,      // c = gelu_tanh(acc + bias) (model dtype)
   EPI_GATE_RES = 2,  // x (float32) += gate[n] * (acc + bias)
-  EPI_STORE_F32 = 3  // c (float32) = acc + bias
+  EPI_STORE_F32 = 3, // c (float32) = acc + bias
+  // EPI_GATE_RES with the float32 stream's read-modify-write marked
+  // non-temporal; chosen by launch_gemm, not by callers
+  EPI_GATE_RES_NT = 4
 };
 
 struct GemmArgs {

@@ -29,7 +29,8 @@ __device__ __forceinline__ void epilogue(const GemmArgs &g, int epi, int64_t row
   switch (epi) {
     case EPI_STORE: st<T>((T *)g.c + o, v); break;
     case EPI_GELU: st<T>((T *)g.c + o, gelu_tanh(v)); break;
-    case EPI_GATE_RES: ((float *)g.c)[o] += g.gate[col] * v; break;
+    case EPI_GATE_RES:
+    case EPI_GATE_RES_NT: ((float *)g.c)[o] += g.gate[col] * v; break;
     default: ((float *)g.c)[o] = v; break;
   }
 }
@@ -158,6 +159,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   // keep C tiles, whose lanes cover 32 consecutive columns of two rows (a full
   // 128-byte line per read-modify-write instruction)
   constexpr bool TR = EPI == EPI_STORE || EPI == EPI_GELU;
+  constexpr bool RES = EPI == EPI_GATE_RES || EPI == EPI_GATE_RES_NT;   // gated residual into the float32 stream
   const GemmArgs g = batch_entry<bf16_t>(g0);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char *sA = smem;                      // [2][BM][128 B]
@@ -427,7 +429,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
     for (int j = 0; j < C::TN; ++j) {
       const int64_t col = n0 + wn * (BN / WN) + j * 32 + lr;
       bvs[j] = bias ? bf2f(bias[col]) : 0.f;
-      gvs[j] = EPI == EPI_GATE_RES ? g.gate[col] : 0.f;
+      gvs[j] = RES ? g.gate[col] : 0.f;
     }
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) {
@@ -441,12 +443,20 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
           // whole 32-row tile inside m (uniform per wave): no per-element guard, so
           // the residual reads go out together (vmcnt also counts stores, and a
           // guarded store per element would serialise every read-modify-write)
-          if (EPI == EPI_GATE_RES) {
+          if constexpr (RES) {
             float xr[16];
+            if constexpr (EPI == EPI_GATE_RES_NT) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) xr[e] = xc[(8 * (e / 4) + (e % 4)) * g.ldc];
+              for (int e = 0; e < 16; ++e) xr[e] = __builtin_nontemporal_load(&xc[(8 * (e / 4) + (e % 4)) * g.ldc]);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = xr[e] + gv * (acc[i][j][e] + bv);
+              for (int e = 0; e < 16; ++e)
+                __builtin_nontemporal_store(xr[e] + gv * (acc[i][j][e] + bv), &xc[(8 * (e / 4) + (e % 4)) * g.ldc]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 16; ++e) xr[e] = xc[(8 * (e / 4) + (e % 4)) * g.ldc];
+#pragma unroll
+              for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = xr[e] + gv * (acc[i][j][e] + bv);
+            }
           } else {
 #pragma unroll
             for (int e = 0; e < 16; ++e) xc[(8 * (e / 4) + (e % 4)) * g.ldc] = acc[i][j][e] + bv;
@@ -458,7 +468,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
           const int64_t row = rb + 8 * (e / 4) + (e % 4);
           if (row >= g.m) continue;
           float *x = (float *)g.c + row * g.ldc + col;
-          if (EPI == EPI_GATE_RES)
+          if (RES)
             *x += gv * (acc[i][j][e] + bv);
           else
             *x = acc[i][j][e] + bv;
@@ -501,6 +511,7 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
     case EPI_STORE: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GELU: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GATE_RES: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>), grid, block, C::LDS_BYTES, s, g); break;
+    case EPI_GATE_RES_NT: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES_NT>), grid, block, C::LDS_BYTES, s, g); break;
     default: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>), grid, block, C::LDS_BYTES, s, g); break;
   }
   return hipGetLastError();
@@ -509,9 +520,10 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
 template <int BM, int BN, int WM, int WN>
 hipError_t set_lds_limit() {
   using C = Cfg<BM, BN, WM, WN>;
-  const void *k[4] = {(const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>,
+  const void *k[5] = {(const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE>,
                       (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>,
                       (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>,
+                      (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES_NT>,
                       (const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>};
   for (const void *f : k) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
@@ -521,8 +533,10 @@ hipError_t set_lds_limit() {
 }
 }  // namespace
 
-hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
+hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
+  GemmArgs g = g_in;
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
+  if (g.epi == EPI_GATE_RES_NT) return hipErrorInvalidValue;   // internal, chosen below
   // the MFMA kernels read 16-byte operand chunks and write 4-column output groups
   const bool aligned = ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0 &&
                        (uintptr_t)g.c % 16 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.bias % 8 == 0 &&
@@ -542,6 +556,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s) {
     // fewer LDS bytes per MFMA (the chip is power-limited under this load).
     // WDC_GEMM_VARIANT=2 selects 16 waves, 0 four waves of 128 x 128.
     static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
+    // Gated residual of a long-K product: the float32 stream's read-modify-write
+    // goes past the caches (non-temporal), which then keep the A and weight
+    // tiles: +7.5% at K = 12,288, +2% at K = 15,360; at K = 3,072 it was 1.5%
+    // slower, so shorter products keep cached accesses.
+    static const int nt = getenv("WDC_GEMM_NT") ? atoi(getenv("WDC_GEMM_NT")) : 1;
+    if (nt && g.epi == EPI_GATE_RES && g.k >= 8192) g.epi = EPI_GATE_RES_NT;
     auto big = [&](const GemmArgs &gg) {
       return variant == 0 ? launch_mfma<256, 256, 2, 2>(gg, s)
              : variant == 1 ? launch_mfma<256, 256, 2, 4>(gg, s)
