@@ -160,6 +160,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   // 128-byte line per read-modify-write instruction)
   constexpr bool TR = EPI == EPI_STORE || EPI == EPI_GELU;
   constexpr bool RES = EPI == EPI_GATE_RES || EPI == EPI_GATE_RES_NT;   // gated residual into the float32 stream
+  constexpr bool STAGE_OUT = BM == 256;   // bf16 output through LDS, whole-line non-temporal stores
   const GemmArgs g = batch_entry<bf16_t>(g0);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char *sA = smem;                      // [2][BM][128 B]
@@ -384,7 +385,46 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
 #undef WDC_GEMM_MFMA1
 
   const bf16_t *bias = (const bf16_t *)g.bias;
-  if constexpr (TR) {
+  if (TR && STAGE_OUT) {
+    // bf16 output staged through LDS (free once the last K stage is consumed:
+    // every read that matters completed before the last stage barrier): each
+    // wave writes its BM/WM x BN/WN tile into its own slice, row-major with the
+    // 16-byte chunk index XOR (row & 7), then reads it back so that every store
+    // instruction writes whole 128-byte row segments, marked non-temporal.
+    constexpr int RB = BN / WN * 2, CPR = RB / 16, RPI = 1024 / RB, WR = BM / WM;
+    static_assert(WR * RB * C::NT / 64 <= C::LDS_BYTES, "staging slices exceed LDS");
+    char *wl = smem + wid * (WR * RB);
+    uint2 bw[C::TN][4];
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        bw[j][q] = bias ? *(const uint2 *)(bias + n0 + wn * (BN / WN) + j * 32 + 4 * lg + 8 * q) : make_uint2(0, 0);
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) {
+        const int r = i * 32 + lr;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float b0 = bf2f((bf16_t)(bw[j][q].x & 0xffff)), b1 = bf2f((bf16_t)(bw[j][q].x >> 16));
+          const float b2 = bf2f((bf16_t)(bw[j][q].y & 0xffff)), b3 = bf2f((bf16_t)(bw[j][q].y >> 16));
+          const uint32_t w0 = pack_bf16(epi_act<EPI>(acc[i][j][4 * q + 0] + b0), epi_act<EPI>(acc[i][j][4 * q + 1] + b1));
+          const uint32_t w1 = pack_bf16(epi_act<EPI>(acc[i][j][4 * q + 2] + b2), epi_act<EPI>(acc[i][j][4 * q + 3] + b3));
+          *(uint2 *)(wl + r * RB + (((4 * j + q) ^ (r & 7)) * 16) + 8 * lg) = make_uint2(w0, w1);
+        }
+      }
+    }
+    typedef __attribute__((ext_vector_type(4))) unsigned u32x4_t;
+#pragma unroll
+    for (int s = 0; s < WR / RPI; ++s) {
+      const int r = s * RPI + lane / CPR, ch = lane % CPR;
+      const u32x4_t v = *(const u32x4_t *)(wl + r * RB + ((ch ^ (r & 7)) * 16));
+      const int64_t row = m0 + wm * WR + r;
+      if (row < g.m)
+        __builtin_nontemporal_store(v, (u32x4_t *)((bf16_t *)g.c + row * g.ldc + n0 + wn * (BN / WN) + ch * 8));
+    }
+  } else if constexpr (TR) {
     // bf16 output: lane (lr, lg) of tile (i, j) holds row lr of the 32x32 output
     // tile and, in accumulator entries 4q..4q+3, the four consecutive columns
     // 8q + 4lg + 0..3, stored as one 8-byte group. The bias of all the lane's
@@ -567,7 +607,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
              : variant == 1 ? launch_mfma<256, 256, 2, 4>(gg, s)
                             : launch_mfma<256, 256, 4, 4>(gg, s);
     };
-    if (g.n % 256 == 0 && g.m >= 512) {
+    // the 256 x 256 kernels stage bf16 outputs through LDS and store whole
+    // 16-byte row chunks: they need 16-byte-aligned output rows (other bf16
+    // outputs take the 128 x 128 kernels, which store 8-byte groups)
+    const bool c16 = g.epi == EPI_STORE || g.epi == EPI_GELU;
+    const bool out16 = !c16 || ((uintptr_t)g.c % 16 == 0 && g.ldc % 8 == 0 && (g.batch <= 1 || g.c_bs % 8 == 0));
+    if (g.n % 256 == 0 && g.m >= 512 && out16) {
       // Tail split for a single large long-K product on a 256-CU device: the
       // rows whose 256 x 256 tiles fill whole dispatch rounds (m1 tiles, a
       // multiple of 256 / gcd(n_tiles, 256)) run as above; the remaining rows,
@@ -587,7 +632,6 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
         g1.m = m1;
         g2.m = g.m - m1;
         g2.a = (const bf16_t *)g.a + m1 * g.lda;
-        const bool c16 = g.epi == EPI_STORE || g.epi == EPI_GELU;
         g2.c = c16 ? (void *)((bf16_t *)g.c + m1 * g.ldc) : (void *)((float *)g.c + m1 * g.ldc);
         hipError_t e = big(g1);
         if (e != hipSuccess) return e;

@@ -49,6 +49,27 @@ def test_linear_matches_oracle(dtype, m, n, k):
     assert err <= (4e-3 if dtype == "bf16" else TOL_F32), err
 
 
+def test_linear_output_rows_not_16_byte_aligned():
+    """bf16 output rows 8-byte but not 16-byte aligned (ldc = n + 4): the
+    product would take the 256 x 256 kernels, whose staged epilogue stores
+    16-byte chunks, so it must run on the 128 x 128 kernels instead. Columns
+    past n stay untouched."""
+    torch = torch_cuda()
+    cfg = synth.get_config("mid")
+    ctx = context(cfg, weights=False)
+    m, n, k = 600, 512, 256
+    rng = _rng(77)
+    a = synth.stored(rng.standard_normal((m, k)), cfg.dtype)
+    w = synth.stored(rng.standard_normal((n, k)) * 0.05, cfg.dtype)
+    b = synth.stored(rng.standard_normal(n) * 0.1, cfg.dtype)
+    out = torch.zeros((m, n + 4), dtype=ctx.tdtype, device="cuda")
+    ctx.linear(ctx.to_device(a), ctx.to_device(w), ctx.to_device(b), out, m, n, k, ldc=n + 4)
+    got = out.float().cpu().numpy()
+    err = rel_l2(got[:, :n], dit.linear({"l.w": w, "l.b": b}, "l", a.astype(np.float64)))
+    assert err <= 4e-3, err
+    assert np.all(got[:, n:] == 0)
+
+
 def test_linear_large_product_rectangle_order():
     """A product big enough for the XCD-rectangle block order (at least 64 chunks
     of 8 x 4 tiles: 65 M tiles in 9 bands, the last one partial, x 32 N tiles),
