@@ -187,9 +187,9 @@ __device__ __forceinline__ void pp_wait4(int n_outstanding) {
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
 }
 
-// Vector phase: Q is scaled by sc = log2(e)/sqrt(HD) once, and -m enters the
-// QK contraction as one more 16-deep slice per 32-key half (ones on the key
-// side, -m as a bf16 pair on the query side), so the matrix phase hands over
+// Vector phase: Q is scaled by sc = log2(e)/sqrt(HD) once, and -m is the
+// accumulator input of the first Q K MFMA of each 32-key half (a lane holds one
+// query, so the tile is -m in all 16 values), so the matrix phase hands over
 // S' = sc Q K^T - m and the vector phase is P = exp2(S'), its bf16 conversion
 // and the row sum of those bf16 values (the weights the PV product uses). m is
 // a reference, not a running max: the first tile's row max, moved to a row's
@@ -199,35 +199,23 @@ __device__ __forceinline__ void pp_wait4(int n_outstanding) {
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 constexpr float PPR_LIMIT = 0x1p64f;
 
-// -m as bf16 (hi, lo) in k-slots 0, 1 of lane group 0; m becomes -(hi + lo)
-__device__ __forceinline__ bf16x8 ppr_mfrag(float &m, int lg) {
-  const __bf16 hi = (__bf16)(-m);
-  const __bf16 lo = (__bf16)(-m - (float)hi);
-  m = -((float)hi + (float)lo);
-  bf16x8 f;
+// accumulator tile that starts a row's Q K contraction at -m
+__device__ __forceinline__ f32x16 ppr_mtile(float m) {
+  f32x16 t;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) f[j] = (__bf16)0.f;
-  if (lg == 0) {
-    f[0] = hi;
-    f[1] = lo;
-  }
-  return f;
+  for (int e = 0; e < 16; ++e) t[e] = -m;
+  return t;
 }
 
 template <int HD>
 __device__ __forceinline__ void ppr_qk(f32x16 (&S)[2], const char *k, const bf16x8 (&qf)[HD / 16],
-                                       const int (&kro)[HD / 16], const bf16x8 &ones, const bf16x8 &mf) {
-  f32x16 zero;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) zero[e] = 0.f;
-  S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, zero, 0, 0, 0);
-  S[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, zero, 0, 0, 0);
+                                       const int (&kro)[HD / 16], const f32x16 &mi) {
 #pragma unroll
   for (int st_ = 0; st_ < HD / 16; ++st_)
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       const bf16x8 kf = *(const bf16x8 *)(k + kro[st_] + kt * 32 * HD * 2);
-      S[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st_], S[kt], 0, 0, 0);
+      S[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st_], st_ == 0 ? mi : S[kt], 0, 0, 0);
     }
 }
 
@@ -258,7 +246,7 @@ __device__ __forceinline__ float ppr_exp(const f32x16 (&S)[2], bf16x8 (&pf)[4]) 
 // above the limit moves the rows to their true max first
 template <int HD>
 __device__ __forceinline__ void ppr_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32x16 (&o)[HD / 32], float &m,
-                                            bf16x8 &mf, float &l, int valid, int lg) {
+                                            f32x16 &mi, float &l, int valid, int lg) {
   if (valid < KV) {                        // partial last tile only: a branch, not selects
     asm volatile("" ::: "memory");
 #pragma unroll
@@ -270,8 +258,8 @@ __device__ __forceinline__ void ppr_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32
   float ls = ppr_exp(S, pf);
   if (__any(ls > PPR_LIMIT)) {
     const float mx = ppr_rowmax(S);
-    float mn = m + (mx > 8.f ? mx : 0.f);
-    mf = ppr_mfrag(mn, lg);
+    const float mn = m + (mx > 8.f ? mx : 0.f);
+    mi = ppr_mtile(mn);
     const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);
     m = mn;
     l *= alpha;
@@ -364,18 +352,11 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  bf16x8 ones;                             // key-side partner of the -m fragment
-#pragma unroll
-  for (int j = 0; j < 8; ++j) ones[j] = (__bf16)0.f;
-  if (lg == 0) {
-    ones[0] = (__bf16)1.f;
-    ones[1] = (__bf16)1.f;
-  }
   float m = 0.f, l = 0.f;
-  bf16x8 mf = ppr_mfrag(m, lg);
+  f32x16 mi = ppr_mtile(m);
   f32x16 S[2];
   bf16x8 pf[4];
-  ppr_qk<HD>(S, smem, qf, kro, ones, mf);
+  ppr_qk<HD>(S, smem, qf, kro, mi);
   {                                        // m = the first tile's row max
     const int v0 = ntiles == 1 ? last_valid : KV;
     if (v0 < KV) {
@@ -386,7 +367,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
           if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= v0) S[kt][e] = -1e30f;
     }
     m = ppr_rowmax(S);
-    mf = ppr_mfrag(m, lg);
+    mi = ppr_mtile(m);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -412,7 +393,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro);                                                 \
-    ppr_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro, ones, mf);                         \
+    ppr_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro, mi);                               \
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);                                           \
     _Pragma("unroll") for (int i_ = 0; i_ < NMF - 4; ++i_) {                                     \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
@@ -420,7 +401,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
     }                                                                                            \
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
     __builtin_amdgcn_sched_barrier(0);                                                           \
-    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mf, l, t + 2 < ntiles ? KV : last_valid, lg); \
+    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mi, l, t + 2 < ntiles ? KV : last_valid, lg); \
     if (grp_a) pp_wait4<HD>(issued);                                                             \
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
   }
@@ -536,18 +517,11 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
   for (int i = 0; i < HD / 32; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  bf16x8 ones;                             // key-side partner of the -m fragment
-#pragma unroll
-  for (int j = 0; j < 8; ++j) ones[j] = (__bf16)0.f;
-  if (lg == 0) {
-    ones[0] = (__bf16)1.f;
-    ones[1] = (__bf16)1.f;
-  }
   float m = 0.f, l = 0.f;
-  bf16x8 mf = ppr_mfrag(m, lg);
+  f32x16 mi = ppr_mtile(m);
   f32x16 S[2][2];                          // S' of tiles t + 1 and t + 2 (index tile & 1)
   bf16x8 pf[2][4];                         // P of tiles t and t + 1 (index tile & 1)
-  ppr_qk<HD>(S[0], smem, qf, kro, ones, mf);
+  ppr_qk<HD>(S[0], smem, qf, kro, mi);
   {                                        // m = the first tile's row max
     const int v0 = ntiles == 1 ? last_valid : KV;
     if (v0 < KV) {
@@ -558,14 +532,14 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
           if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= v0) S[0][kt][e] = -1e30f;
     }
     m = ppr_rowmax(S[0]);
-    mf = ppr_mfrag(m, lg);
+    mi = ppr_mtile(m);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) S[0][kt][e] -= m;
     l = ppr_exp(S[0], pf[0]);
   }
-  if (ntiles > 1) ppr_qk<HD>(S[1], smem + K_BYTES, qf, kro, ones, mf);
+  if (ntiles > 1) ppr_qk<HD>(S[1], smem + K_BYTES, qf, kro, mi);
   // step 0 refills the slot of K_0, which every wave has just read
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
@@ -609,33 +583,26 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     __builtin_amdgcn_sched_barrier(0);                                                           \
     /* One fixed-order stream (unconditional: past the end the Q K reads a stale */              \
     /* K slot and the exponentials a stale S', and neither result is used). MFMA */               \
-    /* q: 0-15 P V (k-step j = q / (HD/32), O tile i = q % (HD/32)), 16-17 the -m */             \
-    /* seeds, 18-33 Q K (hd step (q-18) / 2, key half (q-18) % 2); fragment read r */             \
-    /* (r = q for P V, q - 2 for Q K) goes out four reads ahead of its MFMA; after */             \
-    /* MFMA q < 32 comes exponential q of S'_{t+1}, after every second one the */                 \
-    /* bf16 pair and its row-sum dot product. */                                                  \
-    const char *vb_ = smem + (P) * K_BYTES, *kb_ = smem + (((P) + 2) % NB) * K_BYTES;             \
-    bf16x8 fr_[NMF];                                                                             \
-    float ls = 0.f;                                                                              \
-    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) WDC_PPR3_READ(r_);                          \
-    _Pragma("unroll") for (int q_ = 0; q_ < 34; ++q_) {                                          \
-      if (q_ < 16) {                                                                             \
-        constexpr int NI = HD / 32;                                                              \
-        o[q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_ < 16 ? q_ : 0], pf[n][q_ / NI], o[q_ % NI], 0, 0, 0); \
-      } else if (q_ < 18) {                                                                      \
-        f32x16 z_;                                                                               \
-        _Pragma("unroll") for (int e = 0; e < 16; ++e) z_[e] = 0.f;                              \
-        S[n][q_ - 16] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ones, mf, z_, 0, 0, 0);          \
-      } else {                                                                                   \
-        const int r_ = q_ - 2;                                                                   \
-        S[n][(r_ - 16) % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[r_ >= 16 ? r_ : 16], qf[(r_ - 16) / 2], S[n][(r_ - 16) % 2], 0, 0, 0); \
-      }                                                                                          \
-      __builtin_amdgcn_sched_barrier(0);                                                         \
-      if (q_ < 16 || q_ >= 18) {                                                                 \
-        const int r_ = q_ < 16 ? q_ : q_ - 2;                                                    \
-        if (r_ + 4 < NMF) WDC_PPR3_READ(r_ + 4);                                                 \
-      }                                                                                          \
-      if (q_ < 32) {                                                                             \
+    /* q: 0-15 P V (k-step j = q / (HD/32), O tile i = q % (HD/32)), 16-31 Q K (hd */        \
+    /* step (q-16) / 2, key half q % 2; hd step 0 starts from the -m tile); */               \
+    /* fragment read q goes out four reads ahead of its MFMA; after MFMA q comes */          \
+    /* exponential q of S'_{t+1}, after every second one the bf16 pair and its */            \
+    /* row-sum dot product. */                                                               \
+    const char *vb_ = smem + (P) * K_BYTES, *kb_ = smem + (((P) + 2) % NB) * K_BYTES;        \
+    bf16x8 fr_[NMF];                                                                         \
+    float ls = 0.f;                                                                          \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) WDC_PPR3_READ(r_);                      \
+    _Pragma("unroll") for (int q_ = 0; q_ < NMF; ++q_) {                                     \
+      if (q_ < 16) {                                                                         \
+        constexpr int NI = HD / 32;                                                          \
+        o[q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], pf[n][q_ / NI], o[q_ % NI], 0, 0, 0);\
+      } else {                                                                               \
+        S[n][q_ % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], qf[(q_ - 16) / 2],   \
+                                                               q_ < 18 ? mi : S[n][q_ % 2], 0, 0, 0);\
+      }                                                                                      \
+      __builtin_amdgcn_sched_barrier(0);                                                     \
+      if (q_ + 4 < NMF) WDC_PPR3_READ(q_ + 4);                                               \
+      {                                                                                      \
         const int kt_ = q_ / 16, e_ = q_ % 16;                                                   \
         pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);        \
         if (q_ & 1)                                                                              \
@@ -648,8 +615,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     if (soft) {                                                                                  \
       if (__any(ls > PPR_LIMIT)) {                                                               \
         const float mx = ppr_rowmax(S[c]);                                                       \
-        float mn = m + (mx > 8.f ? mx : 0.f);                                                    \
-        mf = ppr_mfrag(mn, lg);                                                                  \
+        const float mn = m + (mx > 8.f ? mx : 0.f);                                          \
+        mi = ppr_mtile(mn);                                                                  \
         const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);                              \
         m = mn;                                                                                  \
         l *= alpha;                                                                              \
