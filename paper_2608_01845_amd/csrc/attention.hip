@@ -441,8 +441,9 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
 // S and P are double-buffered (S of t + 1 and t + 2, P of t and t + 1). Tile j
 // sits in slot j % 4: step t reads K_{t+2} and V_t, loads K_{t+4} into the
 // slot of K_t (last read in step t - 2, or by the prologue for t = 0, hence
-// one more barrier there) and V_{t+2} into the slot of V_{t-2} (last read in
-// step t - 2).
+// one more barrier there) and V_{t+3} into the slot of V_{t-1} (last read in
+// step t - 1, and waited for before the barrier that ends it); the first four
+// reads of V_{t+1} go out at the end of step t.
 template <int HD>
 __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
   constexpr int QB = 256;                  // 8 waves x 32 queries
@@ -502,12 +503,13 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
                  tile * KV * 2 + i * 32 * (int)a.n_pad * 2);
   };
 
-  if (grp_a) {                             // K_0..K_3, V_0, V_1
+  if (grp_a) {                             // K_0..K_3, V_0..V_2
 #pragma unroll
     for (int j = 0; j < NB; ++j)
       if (j < ntiles) load_k(j, j);
     load_v(0, 0);
     if (ntiles > 1) load_v(1, 1);
+    if (ntiles > 2) load_v(2, 2);
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   }
   __syncthreads();
@@ -545,16 +547,23 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
 
   constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per step
   static_assert(NMF == 32, "the fixed-order step assumes 16 P V and 16 Q K reads (hd 128)");
+  // V^T tiles are loaded three steps ahead, so the tile of step t + 1 is
+  // published by the barrier that ends step t - 1 and step t issues its first
+  // four fragment reads after its own MFMA stream: the next step's first MFMA
+  // finds its operand in registers instead of waiting on LDS after the barrier.
   const bf16x2_t one2_ = {(__bf16)1.f, (__bf16)1.f};
-  // fragment read r of a step: 0-15 V^T (k-step r / (HD/32), O tile r % (HD/32)),
-  // 16-31 K (hd step (r-16) / 2, key half (r-16) % 2)
-#define WDC_PPR3_READ(r)                                                                         \
+  // fragment read r of a step from V^T slot vb and K slot kb: 0-15 V^T (k-step
+  // r / (HD/32), O tile r % (HD/32)), 16-31 K (hd step (r-16) / 2, key half r % 2)
+#define WDC_PPR3_READ(r, vb, kb)                                                                 \
   {                                                                                              \
     if ((r) < 16)                                                                                \
-      fr_[(r)] = *(const bf16x8 *)(vb_ + ((r) % (HD / 32)) * 32 * KV * 2 + vro[(r) / (HD / 32)]); \
+      fr_[(r)] = *(const bf16x8 *)((vb) + ((r) % (HD / 32)) * 32 * KV * 2 + vro[(r) / (HD / 32)]);\
     else                                                                                         \
-      fr_[(r)] = *(const bf16x8 *)(kb_ + kro[((r) >= 16 ? (r) - 16 : 0) / 2] + (((r) - 16) % 2) * 32 * HD * 2); \
+      fr_[(r)] = *(const bf16x8 *)((kb) + kro[((r) >= 16 ? (r) - 16 : 0) / 2] + ((r) % 2) * 32 * HD * 2);\
   }
+  bf16x8 fr_[NMF];
+#pragma unroll
+  for (int r_ = 0; r_ < 4; ++r_) WDC_PPR3_READ(r_, smem, smem);   // step 0's first reads (V^T of tile 0)
   // One tile step with compile-time slot P = t % NB; c = (t + 1) & 1 indexes
   // S' of tile t + 1 and the P it becomes, n = t & 1 the S' of tile t + 2 and
   // the P of tile t.
@@ -568,13 +577,13 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
         load_k((P), t + 4);                                                                      \
         issued += TL::K_STRIPES;                                                                 \
       }                                                                                          \
-      if (t + 2 < ntiles) {                                                                      \
-        load_v(((P) + 2) % NB, t + 2);                                                           \
+      if (t + 3 < ntiles) {                                                                      \
+        load_v(((P) + 3) % NB, t + 3);                                                           \
         issued += TL::V_STRIPES;                                                                 \
       }                                                                                          \
     }                                                                                            \
     const bool soft = t + 1 < ntiles;                                                            \
-    if (t + 2 == ntiles && last_valid < KV) {  /* tile t + 1 is the partial last one */         \
+    if (t + 2 == ntiles && last_valid < KV) {  /* tile t + 1 is the partial last one */          \
       asm volatile("" ::: "memory");                                                             \
       _Pragma("unroll") for (int kt = 0; kt < 2; ++kt)                                           \
       _Pragma("unroll") for (int e = 0; e < 16; ++e)                                             \
@@ -582,32 +591,34 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     /* One fixed-order stream (unconditional: past the end the Q K reads a stale */              \
-    /* K slot and the exponentials a stale S', and neither result is used). MFMA */               \
-    /* q: 0-15 P V (k-step j = q / (HD/32), O tile i = q % (HD/32)), 16-31 Q K (hd */        \
-    /* step (q-16) / 2, key half q % 2; hd step 0 starts from the -m tile); */               \
-    /* fragment read q goes out four reads ahead of its MFMA; after MFMA q comes */          \
-    /* exponential q of S'_{t+1}, after every second one the bf16 pair and its */            \
-    /* row-sum dot product. */                                                               \
-    const char *vb_ = smem + (P) * K_BYTES, *kb_ = smem + (((P) + 2) % NB) * K_BYTES;        \
-    bf16x8 fr_[NMF];                                                                         \
-    float ls = 0.f;                                                                          \
-    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) WDC_PPR3_READ(r_);                      \
-    _Pragma("unroll") for (int q_ = 0; q_ < NMF; ++q_) {                                     \
-      if (q_ < 16) {                                                                         \
-        constexpr int NI = HD / 32;                                                          \
+    /* K slot and the exponentials a stale S', and neither result is used). MFMA */              \
+    /* q: 0-15 P V (k-step j = q / (HD/32), O tile i = q % (HD/32)), 16-31 Q K (hd */            \
+    /* step (q-16) / 2, key half q % 2; hd step 0 starts from the -m tile); */                   \
+    /* fragment read q goes out four reads ahead of its MFMA (reads 0-3 in the */                \
+    /* previous step); after MFMA q comes exponential q of S'_{t+1}, after every */              \
+    /* second one the bf16 pair and its row-sum dot product. */                                  \
+    const char *vb_ = smem + (P) * K_BYTES, *kb_ = smem + (((P) + 2) % NB) * K_BYTES;            \
+    const char *vn_ = smem + (((P) + 1) % NB) * K_BYTES;   /* V^T slot of tile t + 1 */          \
+    float ls = 0.f;                                                                              \
+    _Pragma("unroll") for (int q_ = 0; q_ < NMF; ++q_) {                                         \
+      if (q_ < 16) {                                                                             \
+        constexpr int NI = HD / 32;                                                              \
         o[q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], pf[n][q_ / NI], o[q_ % NI], 0, 0, 0);\
-      } else {                                                                               \
-        S[n][q_ % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], qf[(q_ - 16) / 2],   \
+      } else {                                                                                   \
+        S[n][q_ % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], qf[(q_ - 16) / 2],       \
                                                                q_ < 18 ? mi : S[n][q_ % 2], 0, 0, 0);\
-      }                                                                                      \
-      __builtin_amdgcn_sched_barrier(0);                                                     \
-      if (q_ + 4 < NMF) WDC_PPR3_READ(q_ + 4);                                               \
-      {                                                                                      \
+      }                                                                                          \
+      __builtin_amdgcn_sched_barrier(0);                                                         \
+      if (q_ + 4 < NMF)                                                                          \
+        WDC_PPR3_READ(q_ + 4, vb_, kb_)                                                          \
+      else  /* the next step's first reads: V^T of tile t + 1, published by the last barrier */  \
+        WDC_PPR3_READ(q_ + 4 - NMF, vn_, kb_)                                                    \
+      {                                                                                          \
         const int kt_ = q_ / 16, e_ = q_ % 16;                                                   \
-        pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);        \
+        pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);         \
         if (q_ & 1)                                                                              \
           ls = __builtin_amdgcn_fdot2_f32_bf16(                                                  \
-              bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false); \
+              bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false);\
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \
@@ -615,8 +626,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     if (soft) {                                                                                  \
       if (__any(ls > PPR_LIMIT)) {                                                               \
         const float mx = ppr_rowmax(S[c]);                                                       \
-        const float mn = m + (mx > 8.f ? mx : 0.f);                                          \
-        mi = ppr_mtile(mn);                                                                  \
+        const float mn = m + (mx > 8.f ? mx : 0.f);                                              \
+        mi = ppr_mtile(mn);                                                                      \
         const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);                              \
         m = mn;                                                                                  \
         l *= alpha;                                                                              \
@@ -632,7 +643,9 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
       l += ls;                                                                                   \
     }                                                                                            \
     if (grp_a) pp_wait4<HD>(issued);                                                             \
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
+    /* every older read is done; the four just issued read a slot no load of */                  \
+    /* the next step writes */                                                                   \
+    asm volatile("s_waitcnt lgkmcnt(4)\n\ts_barrier" ::: "memory");                              \
   }
   for (int t0 = 0; t0 < ntiles; t0 += NB) {
     WDC_PPR3_STEP(0)
