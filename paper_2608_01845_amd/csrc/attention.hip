@@ -4,7 +4,8 @@
 // bf16 path (flash attention on the matrix cores, hd = 64 or 128):
 //  * 512-thread blocks of 256 queries, 32 per wavefront, two wavefronts per
 //    SIMD; K tiles [64 keys][hd] and V^T tiles [hd][64 keys] reach LDS by
-//    direct buffer loads, issued two tile steps ahead by four of the waves;
+//    direct buffer loads, issued three or four tile steps ahead by four of the
+//    waves;
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16: the accumulator of a 32x32
 //    tile gives lane l one query (l % 32) and 16 keys, so a query's row
 //    statistics live in one lane and its partner l ^ 32 (one exchange);
@@ -143,18 +144,22 @@ struct TileLoad {
   }
 };
 
-// O^T += V^T P^T for one tile: the V^T fragment (O tile i, k-step j) is read
-// right before its MFMA.
+// V^T fragment f (k-step j = f / (HD/32), O tile i = f % (HD/32)) of a tile
+template <int HD>
+__device__ __forceinline__ bf16x8 pp_vfrag(const char *v, const int (&vro)[4], int f) {
+  return *(const bf16x8 *)(v + (f % (HD / 32)) * 32 * KV * 2 + vro[f / (HD / 32)]);
+}
+
+// O^T += V^T P^T for one tile: fragments 0-3 come read (in the previous
+// step), the others are read right before their MFMAs.
 template <int HD>
 __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const bf16x8 (&pf)[4],
-                                      const int (&vro)[4]) {
+                                      const int (&vro)[4], const bf16x8 (&pre)[4]) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i) {
-      const bf16x8 vf = *(const bf16x8 *)(v + i * 32 * KV * 2 + vro[j]);
-      o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j], o[i], 0, 0, 0);
-    }
+  for (int f = 0; f < 4 * (HD / 32); ++f) {
+    const bf16x8 vf = f < 4 ? pre[f < 4 ? f : 0] : pp_vfrag<HD>(v, vro, f);
+    o[f % (HD / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[f / (HD / 32)], o[f % (HD / 32)], 0, 0, 0);
+  }
 }
 
 // Reference-max kernel (ppr), the two-phase form. 8 wavefronts per block (two
@@ -166,15 +171,17 @@ __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const
 // of a SIMD drift apart and one's vector phase overlaps the other's MFMAs (a
 // ping-pong with a barrier between the phases was 4.6% slower at hd 128 and 11%
 // at hd 64 on the same box).
-// Pipeline: group A (waves 0-3) issues the loads of K_{t+3} and V_{t+2} in step
-// t, two steps before they are read, and at the end of step t waits only for
-// the loads of step t-1 (a partial vmcnt), so a tile load has two full steps to
-// land. The step loop is unrolled by four so every LDS fragment address is a
-// per-lane register plus an immediate offset. Buffer reuse: step t reads V_t
-// and K_{t+1}; K_{t+3} overwrites K_{t-1}, last read in step t-2, and V_{t+2}
-// overwrites V_{t-2}, last read in step t-2; each wave drains its LDS reads
-// before the barrier that ends a step, so both were free two barriers before
-// the loads are issued.
+// Pipeline: group A (waves 0-3) issues the loads of K_{t+3} and V_{t+3} in step
+// t and at the end of step t waits only for the loads of step t-1 (a partial
+// vmcnt), so a tile load has at least two full steps to land. The first four
+// V^T fragment reads of step t+1 go out right after step t's matrix phase
+// (V_{t+1} was published by the barrier that ended step t-1) and land during
+// its vector phase. The step loop is unrolled by four so every LDS fragment
+// address is a per-lane register plus an immediate offset. Buffer reuse: step
+// t reads V_t and K_{t+1}; K_{t+3} overwrites K_{t-1}, last read in step t-2,
+// and V_{t+3} overwrites V_{t-1}, last read in step t-1; before the barrier
+// that ends a step each wave waits for all its LDS reads but the four early
+// ones, whose slot no load of the next step writes.
 template <int HD>
 __device__ __forceinline__ void pp_wait4(int n_outstanding) {
   constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
@@ -342,7 +349,10 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
       load_k(1, 1);
       load_v(1, 1);
     }
-    if (ntiles > 2) load_k(2, 2);
+    if (ntiles > 2) {
+      load_k(2, 2);
+      load_v(2, 2);
+    }
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   }
   __syncthreads();
@@ -376,6 +386,9 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   }
 
   constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per matrix phase
+  bf16x8 pre[4];                           // first four V^T fragments of the next P V
+#pragma unroll
+  for (int f = 0; f < 4; ++f) pre[f] = pp_vfrag<HD>(smem, vro, f);
   // One tile step with compile-time buffer slot P = t % NB.
 #define WDC_PPR_STEP(P)                                                                          \
   {                                                                                              \
@@ -386,24 +399,30 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
         load_k(((P) + 3) % NB, t + 3);                                                           \
         issued += TL::K_STRIPES;                                                                 \
       }                                                                                          \
-      if (t + 2 < ntiles) {                                                                      \
-        load_v(((P) + 2) % NB, t + 2);                                                           \
+      if (t + 3 < ntiles) {                                                                      \
+        load_v(((P) + 3) % NB, t + 3);                                                           \
         issued += TL::V_STRIPES;                                                                 \
       }                                                                                          \
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
-    pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro);                                                 \
+    pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro, pre);                                            \
     ppr_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro, mi);                               \
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);                                           \
     _Pragma("unroll") for (int i_ = 0; i_ < NMF - 4; ++i_) {                                     \
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                         \
     }                                                                                            \
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
     __builtin_amdgcn_sched_barrier(0);                                                           \
-    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mi, l, t + 2 < ntiles ? KV : last_valid, lg); \
+    /* the next P V's first fragments (V^T of tile t + 1, published by the last */               \
+    /* barrier) land during the vector phase */                                                  \
+    _Pragma("unroll") for (int f_ = 0; f_ < 4; ++f_)                                             \
+      pre[f_] = pp_vfrag<HD>(smem + (((P) + 1) % NB) * K_BYTES, vro, f_);                        \
+    __builtin_amdgcn_sched_barrier(0);                                                           \
+    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mi, l, t + 2 < ntiles ? KV : last_valid, lg);\
     if (grp_a) pp_wait4<HD>(issued);                                                             \
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");                             \
+    /* every older read is done; the four just issued read a slot no load of */                  \
+    /* the next step writes */                                                                   \
+    asm volatile("s_waitcnt lgkmcnt(4)\n\ts_barrier" ::: "memory");                              \
   }
   for (int t0 = 0; t0 < ntiles; t0 += NB) {
     WDC_PPR_STEP(0)
