@@ -182,6 +182,33 @@ __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const
 // and V_{t+3} overwrites V_{t-1}, last read in step t-1; before the barrier
 // that ends a step each wave waits for all its LDS reads but the four early
 // ones, whose slot no load of the next step writes.
+// Buffering of the two-phase kernel. hd 128: four K and four V^T slots (128 KB),
+// tiles loaded three steps ahead, a barrier after every step. hd 64 (8 KB
+// tiles): eight slots, tiles loaded six steps ahead and a barrier after every
+// second step, which halves the fixed per-step cost of the short hd 64 step.
+// Slot reuse at hd 64: the load in step t overwrites tile t - 2, whose last
+// reads (V in step t - 2, K in step t - 3) precede the barrier before step t;
+// the barrier after step b waits for the loads of steps up to b - 2, so the
+// tiles step t reads (K_{t+1} and V_t, loaded in steps t - 5 and t - 6) and the
+// early V^T reads are published in time.
+template <int HD> struct PprShape;
+template <> struct PprShape<128> { static constexpr int NB = 4, LEAD = 3, BSTEP = 1; };
+template <> struct PprShape<64> { static constexpr int NB = 8, LEAD = 6, BSTEP = 2; };
+
+// vmcnt wait leaving n of this wave's tile loads in flight (n: loads of the
+// last one or two steps)
+template <int HD>
+__device__ __forceinline__ void ppr_vm_wait(int n) {
+  constexpr int S1 = TileLoad<HD>::K_STRIPES + TileLoad<HD>::V_STRIPES;
+  static_assert(PprShape<HD>::BSTEP * S1 < 16, "vmcnt immediate");
+  if (PprShape<HD>::BSTEP == 2 && n == 2 * S1)
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | ((2 * S1) & 15));
+  else if (n == S1)
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | S1);
+  else
+    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
+}
+
 template <int HD>
 __device__ __forceinline__ void pp_wait4(int n_outstanding) {
   constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
@@ -286,7 +313,9 @@ __device__ __forceinline__ void ppr_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32
 template <int HD>
 __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   constexpr int QB = 256;                  // 8 waves x 32 queries
-  constexpr int NB = 4;                    // K buffers and V^T buffers
+  constexpr int NB = PprShape<HD>::NB;     // K buffers and V^T buffers
+  constexpr int LEAD = PprShape<HD>::LEAD; // tiles between a load and its step
+  constexpr int BSTEP = PprShape<HD>::BSTEP;   // tile steps per block barrier
   constexpr int K_BYTES = KV * HD * 2;
   constexpr int V_BASE = NB * K_BYTES;     // V^T buffers follow the K buffers
   using TL = TileLoad<HD>;
@@ -343,16 +372,12 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   };
 
   if (grp_a) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (ntiles > 1) {
-      load_k(1, 1);
-      load_v(1, 1);
-    }
-    if (ntiles > 2) {
-      load_k(2, 2);
-      load_v(2, 2);
-    }
+#pragma unroll
+    for (int j = 0; j < LEAD; ++j)
+      if (j < ntiles) {
+        load_k(j, j);
+        load_v(j, j);
+      }
     __builtin_amdgcn_s_waitcnt(WAIT_VM0);
   }
   __syncthreads();
@@ -387,6 +412,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
 
   constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per matrix phase
   bf16x8 pre[4];                           // first four V^T fragments of the next P V
+  int iss_prev = 0;                        // loads issued in the step before (no barrier after it)
 #pragma unroll
   for (int f = 0; f < 4; ++f) pre[f] = pp_vfrag<HD>(smem, vro, f);
   // One tile step with compile-time buffer slot P = t % NB.
@@ -394,15 +420,10 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
   {                                                                                              \
     const int t = t0 + (P);                                                                      \
     int issued = 0;                                                                              \
-    if (grp_a) {                                                                                 \
-      if (t + 3 < ntiles) {                                                                      \
-        load_k(((P) + 3) % NB, t + 3);                                                           \
-        issued += TL::K_STRIPES;                                                                 \
-      }                                                                                          \
-      if (t + 3 < ntiles) {                                                                      \
-        load_v(((P) + 3) % NB, t + 3);                                                           \
-        issued += TL::V_STRIPES;                                                                 \
-      }                                                                                          \
+    if (grp_a && t + LEAD < ntiles) {                                                            \
+      load_k(((P) + LEAD) % NB, t + LEAD);                                                       \
+      load_v(((P) + LEAD) % NB, t + LEAD);                                                       \
+      issued = TL::K_STRIPES + TL::V_STRIPES;                                                    \
     }                                                                                            \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro, pre);                                            \
@@ -419,10 +440,16 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
       pre[f_] = pp_vfrag<HD>(smem + (((P) + 1) % NB) * K_BYTES, vro, f_);                        \
     __builtin_amdgcn_sched_barrier(0);                                                           \
     if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mi, l, t + 2 < ntiles ? KV : last_valid, lg);\
-    if (grp_a) pp_wait4<HD>(issued);                                                             \
-    /* every older read is done; the four just issued read a slot no load of */                  \
-    /* the next step writes */                                                                   \
-    asm volatile("s_waitcnt lgkmcnt(4)\n\ts_barrier" ::: "memory");                              \
+    if ((P) % BSTEP == BSTEP - 1) {                                                              \
+      /* only the loads of the last BSTEP steps may still be in flight; every                    \
+         older read is done, and the four just issued read a slot no load of                     \
+         the next LEAD - 1 steps writes */                                                       \
+      if (grp_a) ppr_vm_wait<HD>(iss_prev + issued);                                             \
+      asm volatile("s_waitcnt lgkmcnt(4)\n\ts_barrier" ::: "memory");                            \
+      iss_prev = 0;                                                                              \
+    } else {                                                                                     \
+      iss_prev = issued;                                                                         \
+    }                                                                                            \
   }
   for (int t0 = 0; t0 < ntiles; t0 += NB) {
     WDC_PPR_STEP(0)
@@ -432,6 +459,16 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
     WDC_PPR_STEP(2)
     if (t0 + 3 >= ntiles) break;
     WDC_PPR_STEP(3)
+    if constexpr (NB == 8) {
+      if (t0 + 4 >= ntiles) break;
+      WDC_PPR_STEP(4)
+      if (t0 + 5 >= ntiles) break;
+      WDC_PPR_STEP(5)
+      if (t0 + 6 >= ntiles) break;
+      WDC_PPR_STEP(6)
+      if (t0 + 7 >= ntiles) break;
+      WDC_PPR_STEP(7)
+    }
   }
 #undef WDC_PPR_STEP
 
@@ -710,7 +747,7 @@ hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
 
 template <int HD>
 hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
-  constexpr int LDS = 2 * 4 * KV * HD * 2;     // four K tiles, four V^T tiles
+  constexpr int LDS = 2 * PprShape<HD>::NB * KV * HD * 2;   // K tiles and V^T tiles
   static bool seen[64] = {};
   if (first_on_device(seen)) {
     const hipError_t e = hipFuncSetAttribute((const void *)k_attn_bf16_ppr<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
