@@ -171,9 +171,10 @@ __device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const
 // of a SIMD drift apart and one's vector phase overlaps the other's MFMAs (a
 // ping-pong with a barrier between the phases was 4.6% slower at hd 128 and 11%
 // at hd 64 on the same box).
-// Pipeline: group A (waves 0-3) issues the loads of K_{t+3} and V_{t+3} in step
-// t and at the end of step t waits only for the loads of step t-1 (a partial
-// vmcnt), so a tile load has at least two full steps to land. The first four
+// Pipeline (hd 128; hd 64 differs as PprShape below states): group A (waves
+// 0-3) issues the loads of K_{t+3} and V_{t+3} in step t and at the end of step
+// t waits only for the loads of step t-1 (a partial vmcnt), so a tile load has
+// at least two full steps to land. The first four
 // V^T fragment reads of step t+1 go out right after step t's matrix phase
 // (V_{t+1} was published by the barrier that ended step t-1) and land during
 // its vector phase. The step loop is unrolled by four so every LDS fragment
