@@ -32,7 +32,7 @@ PEAK_HBM_GBS = 8000.0
 # copy; profiles/attention_13b_hbm_traffic.md). Valid only for the kernel
 # version named here; set to None whenever that kernel changes.
 MEASURED_TRAFFIC = {"k_attn_bf16_ppr3<128>": 8.306e9}
-ATTN_KERNEL = {128: "k_attn_bf16_ppr3<128>", 64: "k_attn_bf16_ppr<64>"}   # default bf16 kernel by head size
+ATTN_KERNEL = {128: "k_attn_bf16_ppr3<128>", 64: "k_attn_bf16_ppr3<64>"}   # default bf16 kernel by head size
 METRIC = "DiT fwd TFLOP/s (% bf16 MFMA peak) + denoising steps/s at 13B shape"
 
 

@@ -14,9 +14,9 @@
 //    bf16 k-values, and the V^T operand is read with the same key order, so P
 //    never goes through LDS;
 //  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr3, the
-//    default at hd 128, whose step runs the vector work of tile t + 1 inside
-//    the MFMA stream of tiles t and t + 2; k_attn_bf16_ppr, the two-phase form
-//    and the default at hd 64).
+//    default, whose step runs the vector work of tile t + 1 inside the MFMA
+//    stream of tiles t and t + 2; k_attn_bf16_ppr, the two-phase form, kept
+//    for comparison).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
@@ -603,20 +603,23 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
   constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per step
-  static_assert(NMF == 32, "the fixed-order step assumes 16 P V and 16 Q K reads (hd 128)");
+  static_assert(NMF == 16 || NMF == 32, "hd 64 or 128");
+  constexpr int NPV = NMF / 2;             // P V reads (and MFMAs) per step; as many Q K
+  constexpr int EPM = 32 / NMF;            // exponentials after each MFMA (32 per step)
   // V^T tiles are loaded three steps ahead, so the tile of step t + 1 is
   // published by the barrier that ends step t - 1 and step t issues its first
   // four fragment reads after its own MFMA stream: the next step's first MFMA
   // finds its operand in registers instead of waiting on LDS after the barrier.
   const bf16x2_t one2_ = {(__bf16)1.f, (__bf16)1.f};
-  // fragment read r of a step from V^T slot vb and K slot kb: 0-15 V^T (k-step
-  // r / (HD/32), O tile r % (HD/32)), 16-31 K (hd step (r-16) / 2, key half r % 2)
+  // fragment read r of a step from V^T slot vb and K slot kb: r < NPV V^T (k-step
+  // r / (HD/32), O tile r % (HD/32)), then K (hd step (r-NPV) / 2, key half (r-NPV) % 2)
 #define WDC_PPR3_READ(r, vb, kb)                                                                 \
   {                                                                                              \
-    if ((r) < 16)                                                                                \
+    if ((r) < NPV)                                                                               \
       fr_[(r)] = *(const bf16x8 *)((vb) + ((r) % (HD / 32)) * 32 * KV * 2 + vro[(r) / (HD / 32)]);\
     else                                                                                         \
-      fr_[(r)] = *(const bf16x8 *)((kb) + kro[((r) >= 16 ? (r) - 16 : 0) / 2] + ((r) % 2) * 32 * HD * 2);\
+      fr_[(r)] = *(const bf16x8 *)((kb) + kro[((r) >= NPV ? (r) - NPV : 0) / 2] +                \
+                                   (((r) >= NPV ? (r) - NPV : 0) % 2) * 32 * HD * 2);            \
   }
   bf16x8 fr_[NMF];
 #pragma unroll
@@ -658,22 +661,23 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     const char *vn_ = smem + (((P) + 1) % NB) * K_BYTES;   /* V^T slot of tile t + 1 */          \
     float ls = 0.f;                                                                              \
     _Pragma("unroll") for (int q_ = 0; q_ < NMF; ++q_) {                                         \
-      if (q_ < 16) {                                                                             \
+      if (q_ < NPV) {                                                                            \
         constexpr int NI = HD / 32;                                                              \
         o[q_ % NI] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], pf[n][q_ / NI], o[q_ % NI], 0, 0, 0);\
       } else {                                                                                   \
-        S[n][q_ % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], qf[(q_ - 16) / 2],       \
-                                                               q_ < 18 ? mi : S[n][q_ % 2], 0, 0, 0);\
+        const int g_ = q_ >= NPV ? q_ - NPV : 0;                                                 \
+        S[n][g_ % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr_[q_], qf[g_ / 2],              \
+                                                               g_ < 2 ? mi : S[n][g_ % 2], 0, 0, 0);\
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
       if (q_ + 4 < NMF)                                                                          \
         WDC_PPR3_READ(q_ + 4, vb_, kb_)                                                          \
       else  /* the next step's first reads: V^T of tile t + 1, published by the last barrier */  \
         WDC_PPR3_READ(q_ + 4 - NMF, vn_, kb_)                                                    \
-      {                                                                                          \
-        const int kt_ = q_ / 16, e_ = q_ % 16;                                                   \
+      _Pragma("unroll") for (int x_ = 0; x_ < EPM; ++x_) {                                       \
+        const int ei_ = q_ * EPM + x_, kt_ = ei_ / 16, e_ = ei_ % 16;                            \
         pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);         \
-        if (q_ & 1)                                                                              \
+        if (ei_ & 1)                                                                             \
           ls = __builtin_amdgcn_fdot2_f32_bf16(                                                  \
               bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false);\
       }                                                                                          \
@@ -767,18 +771,16 @@ hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    // Default: the 8-wave reference-max kernel with four-deep tile buffers and
-    // one barrier per tile, in its three-stage form at hd 128 (ppr3: 3.5-4.5%
-    // faster than the two-phase ppr at the 13B shape) and its two-phase form at
-    // hd 64 (the fixed-order stream is written for hd 128).
-    // WDC_ATTN_VARIANT=4 selects ppr at hd 128 too, for comparison.
+    // Default: the 8-wave reference-max kernel in its three-stage form (ppr3:
+    // 3.5-4.5% faster than the two-phase ppr at the 13B shape, about 2.5% at
+    // hd 64). WDC_ATTN_VARIANT=4 selects the two-phase ppr, for comparison.
     static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 5;
     static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
     AttnArgs b = a;
     b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
     if (a.hd == 128)
       return variant == 4 ? launch_bf16_ppr<128>(b, s) : launch_bf16_ppr3<128>(b, s);
-    if (a.hd == 64) return launch_bf16_ppr<64>(b, s);
+    if (a.hd == 64) return variant == 4 ? launch_bf16_ppr<64>(b, s) : launch_bf16_ppr3<64>(b, s);
     return hipErrorInvalidValue;
   }
   dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);

@@ -3,7 +3,7 @@
 The library reads its comparison switches (WDC_GEMM_VARIANT, WDC_ATTN_VARIANT,
 ...) once per process, so tests/test_gpu_switches.py starts this script with
 the switch in its environment. It checks the bf16 GEMM on products that take
-the 256 x 256 block tiles, or the bf16 attention at hd 128, against the oracle
+the 256 x 256 block tiles, or the bf16 attention at hd 64 and 128, against the oracle
 and exits non-zero on a mismatch.
 """
 import os
@@ -41,18 +41,19 @@ def check_gemm() -> float:
 def check_attention() -> float:
     from tests.test_gpu_kernels import _attn_inputs
     torch = torch_cuda()
-    cfg = small_cfg("bf16", head_dim=128)
-    ctx = context(cfg, weights=False)
-    heads = cfg.heads
     worst = 0.0
-    for n in (61, 100, 700, 1111):
-        (q, k, v), (qd, kd, vd) = _attn_inputs(ctx, heads, 128, n, seed=n, bf16=True)
-        out = torch.zeros((n, heads * 128), dtype=torch.bfloat16, device="cuda")
-        ctx.attention(qd, kd, vd, n, out, heads * 128)
-        ref = dit.attention(q, k, v).transpose(1, 0, 2).reshape(n, heads * 128)
-        err = rel_l2(out.float().cpu().numpy(), ref)
-        print(f"attention hd 128 n {n}: rel_l2 {err:.2e}", flush=True)
-        worst = max(worst, err)
+    for hd in (64, 128):
+        cfg = small_cfg("bf16", head_dim=hd)
+        ctx = context(cfg, weights=False)
+        heads = cfg.heads
+        for n in (61, 100, 700, 1111):
+            (q, k, v), (qd, kd, vd) = _attn_inputs(ctx, heads, hd, n, seed=n, bf16=True)
+            out = torch.zeros((n, heads * hd), dtype=torch.bfloat16, device="cuda")
+            ctx.attention(qd, kd, vd, n, out, heads * hd)
+            ref = dit.attention(q, k, v).transpose(1, 0, 2).reshape(n, heads * hd)
+            err = rel_l2(out.float().cpu().numpy(), ref)
+            print(f"attention hd {hd} n {n}: rel_l2 {err:.2e}", flush=True)
+            worst = max(worst, err)
     return worst
 
 

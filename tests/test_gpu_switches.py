@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.mark.parametrize("switch,value,kind", [
     ("WDC_GEMM_VARIANT", "2", "gemm"),   # 16 waves of 64 x 64
     ("WDC_GEMM_VARIANT", "0", "gemm"),   # 4 waves of 128 x 128
-    ("WDC_ATTN_VARIANT", "4", "attn"),   # two-phase reference-max kernel at hd 128
+    ("WDC_ATTN_VARIANT", "4", "attn"),   # two-phase reference-max kernel at hd 64 and 128
 ])
 def test_switch_matches_oracle(switch, value, kind):
     env = dict(os.environ, **{switch: value})
