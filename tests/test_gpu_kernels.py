@@ -149,8 +149,9 @@ def _attn_device(ctx, q, k, v, bf16):
     return qd, kd, vd
 
 
-@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 700), (64, 61), (128, 512), (128, 1000), (128, 129),
-                                        (128, 320), (128, 1111), (128, 61), (128, 100), (128, 256)])
+@pytest.mark.parametrize("head_dim,n", [(64, 256), (64, 700), (64, 61), (64, 100), (64, 150), (64, 449),
+                                        (128, 512), (128, 1000), (128, 129), (128, 320), (128, 1111), (128, 61),
+                                        (128, 100), (128, 150), (128, 256)])
 def test_attention_bf16_matches_oracle(head_dim, n):
     torch = torch_cuda()
     cfg = small_cfg("bf16", head_dim=head_dim)
