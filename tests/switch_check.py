@@ -46,7 +46,8 @@ def check_attention() -> float:
         cfg = small_cfg("bf16", head_dim=hd)
         ctx = context(cfg, weights=False)
         heads = cfg.heads
-        for n in (61, 100, 700, 1111):
+        # 1, 2, 7, 8, 11 and 18 key tiles (the hd 64 two-phase form loads six ahead over eight slots)
+        for n in ((61, 100, 385, 449, 700, 1111) if hd == 64 else (61, 100, 700, 1111)):
             (q, k, v), (qd, kd, vd) = _attn_inputs(ctx, heads, hd, n, seed=n, bf16=True)
             out = torch.zeros((n, heads * hd), dtype=torch.bfloat16, device="cuda")
             ctx.attention(qd, kd, vd, n, out, heads * hd)
