@@ -315,3 +315,99 @@ def test_forward_final_layer_and_conditioning():
     v1 = dit.final_layer(W, cfg, x[: cfg.n_video], cemb)
     x[cfg.n_video:] += 100
     np.testing.assert_array_equal(dit.final_layer(W, cfg, x[: cfg.n_video], cemb), v1)
+
+
+# --------------------------------------------------------------------------- whole F_theta vs torch
+
+def torch_forward(W, cfg, z, t, cond=None, text=None, cam=None):
+    """Independent composition of F_theta from torch library ops: the patch
+    embedding as a strided 3D convolution, the blocks of ``torch_block``, the
+    output head by torch LayerNorm / SiLU / linear and unpatchify by einops."""
+    import einops
+    d, half = cfg.hidden, 128
+    lin = lambda n, y: tF.linear(y, T(W[n + ".w"]), T(W[n + ".b"]))
+    freqs = torch.exp(-math.log(10000.0) * torch.arange(half, dtype=torch.float64) / half)
+    ang = 1000.0 * t * freqs
+    c = lin("t_embed.fc2", tF.silu(lin("t_embed.fc1", torch.cat([torch.cos(ang), torch.sin(ang)]))))
+    if cfg.cond_dim:
+        c = c + lin("cond_embed", T(cond))
+    if cfg.cam_dim:
+        c = c + lin("cam_embed", T(cam))
+    ch = cfg.latent[0]
+    kern = T(W["patch_embed.w"]).reshape(d, ch, *cfg.patch)
+    x = tF.conv3d(T(z)[None], kern, T(W["patch_embed.b"]), stride=tuple(cfg.patch))[0]   # [D, F', H', W']
+    x = x.reshape(d, -1).T
+    if cfg.text_tokens:
+        x = torch.cat([x, lin("text_proj", T(text))])
+    for b in range(cfg.n_blocks):
+        x = T(torch_block(W, cfg, b, x.numpy(), c.numpy()))
+    shift, scale = lin("final.ada", tF.silu(c)).chunk(2)
+    h = tF.layer_norm(x[: cfg.n_video], (d,), eps=1e-6) * (1 + scale) + shift
+    out = lin("final.lin", h)
+    fp, hp, wp = cfg.grid
+    pt, ph, pw = cfg.patch
+    return einops.rearrange(out.numpy(), "(f h w) (c a i j) -> c (f a) (h i) (w j)", f=fp, h=hp, w=wp,
+                            c=ch, a=pt, i=ph, j=pw)
+
+
+def _forward_case(**kw):
+    cfg = small_cfg(**kw)
+    W = {k: v.astype(np.float64) * 5 for k, v in synth.gen_weights(cfg).items()}    # visible modulation
+    inp = synth.gen_inputs(cfg)
+    return cfg, W, inp
+
+
+@pytest.mark.parametrize("patch,t", [((1, 2, 2), 0.62), ((2, 2, 2), 0.25)])
+def test_dit_forward_matches_torch_composition(patch, t):
+    """The whole F_theta (conditioning, patch embedding, all three block kinds
+    over the joint sequence, the output head and unpatchify) against the torch
+    composition."""
+    cfg, W, inp = _forward_case(patch=patch)
+    got = dit.dit_forward(W, cfg, inp["z_T"], t, inp["cond"], inp["text"], inp["cam"])
+    ref = torch_forward(W, cfg, inp["z_T"], t, inp["cond"], inp["text"], inp["cam"])
+    assert np.abs(ref).max() > 1e-2
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-10 * np.abs(ref).max())
+
+
+def _final_swapped(W, cfg, x_video, c_emb):
+    scale, shift = np.split(dit.linear(W, "final.ada", dit.silu(c_emb)), 2)
+    out = dit.linear(W, "final.lin", dit.modulate(dit.layer_norm(x_video), shift, scale))
+    return dit.unpatchify(out, cfg.latent, cfg.patch)
+
+
+def _final_no_silu(W, cfg, x_video, c_emb):
+    shift, scale = np.split(dit.linear(W, "final.ada", c_emb), 2)
+    out = dit.linear(W, "final.lin", dit.modulate(dit.layer_norm(x_video), shift, scale))
+    return dit.unpatchify(out, cfg.latent, cfg.patch)
+
+
+def _final_no_norm(W, cfg, x_video, c_emb):
+    shift, scale = np.split(dit.linear(W, "final.ada", dit.silu(c_emb)), 2)
+    out = dit.linear(W, "final.lin", dit.modulate(x_video, shift, scale))
+    return dit.unpatchify(out, cfg.latent, cfg.patch)
+
+
+@pytest.mark.parametrize("mistake", [_final_swapped, _final_no_silu, _final_no_norm])
+def test_output_head_mistakes_are_caught(monkeypatch, mistake):
+    """Plausible mistakes planted in the oracle's output head (shift and scale
+    swapped, SiLU dropped, LayerNorm dropped) make it disagree with the torch
+    composition, so the comparison above pins the head."""
+    cfg, W, inp = _forward_case()
+    ref = torch_forward(W, cfg, inp["z_T"], 0.62, inp["cond"], inp["text"], inp["cam"])
+    monkeypatch.setattr(dit, "final_layer", mistake)
+    bad = dit.dit_forward(W, cfg, inp["z_T"], 0.62, inp["cond"], inp["text"], inp["cam"])
+    assert np.abs(bad - ref).max() > 1e-3 * np.abs(ref).max()
+
+
+def test_output_head_matches_torch():
+    """The output head alone: torch LayerNorm, SiLU and linear, then einops unpatchify."""
+    import einops
+    cfg, W, inp = _forward_case()
+    x = RNG.standard_normal((cfg.n_video, cfg.hidden)) * 2 + 0.5
+    c = RNG.standard_normal(cfg.hidden)
+    shift, scale = tF.linear(tF.silu(T(c)), T(W["final.ada.w"]), T(W["final.ada.b"])).chunk(2)
+    h = tF.layer_norm(T(x), (cfg.hidden,), eps=1e-6) * (1 + scale) + shift
+    out = tF.linear(h, T(W["final.lin.w"]), T(W["final.lin.b"])).numpy()
+    fp, hp, wp = cfg.grid
+    ref = einops.rearrange(out, "(f h w) (c a i j) -> c (f a) (h i) (w j)", f=fp, h=hp, w=wp, c=16, a=1, i=2, j=2)
+    np.testing.assert_allclose(dit.final_layer(W, cfg, x, c), ref, atol=1e-12 * np.abs(ref).max())
