@@ -228,6 +228,21 @@ wdc_status wdc_scheduler_step(wdc_ctx *ctx, const float *d_z, const float *d_v, 
 wdc_status wdc_surrogate_step(wdc_ctx *ctx, wdc_state *st, const float *d_z, int32_t k, int32_t S, float *d_zhat,
                               wdc_step_log *h_log);
 
+/* wdc_surrogate_step for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same kernels, host arithmetic, results and state update, with the
+ * statistics kernels' partial sums and float64 reductions kept in one fixed
+ * device array of the library (337,920 bytes per device, held until the
+ * process ends) instead of the state's memory. It makes no device or pinned
+ * host allocation and records no timing events. That array is shared by every
+ * call on the device and keeps the last call's contents (each call overwrites
+ * what it reads): calls that overlap on one device, from several streams or
+ * threads, race. A latent whose statistics would not fit the array is
+ * rejected with WDC_E_WORKSPACE (none does: 16 channels x 8 segments x 64
+ * slices is the largest plan). Synchronises the stream like wdc_surrogate_step. */
+wdc_status wdc_surrogate_step_noalloc(wdc_ctx *ctx, wdc_state *st, const float *d_z, int32_t k, int32_t S,
+                                      float *d_zhat, wdc_step_log *h_log);
+
 /* Transition risk controller, Eq. (6)-(10).
  * PRE_DECISION (after wdc_surrogate_step of the same k): proxy p_k, weight w_k,
  *   R_cand, availability and the decision; h_log->exact = 1 means Exact.

@@ -111,6 +111,7 @@ def load() -> C.CDLL:
         "wdc_dit_forward_batch": (i32, [vp, i32, vp, dbl, vp, vp, vp, vp]),
         "wdc_scheduler_step": (i32, [vp, vp, vp, dbl, dbl, vp, i64]),
         "wdc_surrogate_step": (i32, [vp, vp, vp, i32, i32, vp, C.POINTER(StepLog)]),
+        "wdc_surrogate_step_noalloc": (i32, [vp, vp, vp, i32, i32, vp, C.POINTER(StepLog)]),
         "wdc_risk_update": (i32, [vp, vp, i32, i32, i32, vp, vp, C.POINTER(StepLog)]),
         "wdc_rollout": (i32, [vp, vp, vp, i32, vp, vp, vp, i32, C.POINTER(C.c_uint8), vp, C.POINTER(C.c_uint8),
                               C.POINTER(StepLog)]),
@@ -136,7 +137,7 @@ def exported_symbols() -> List[str]:
         "wdc_weight_info", "wdc_bind_weights", "wdc_init_weights_random", "wdc_workspace_bytes", "wdc_bind_workspace",
         "wdc_state_bytes", "wdc_state_create", "wdc_state_reset", "wdc_state_destroy", "wdc_state_bank_slot",
         "wdc_cond_embed", "wdc_dit_block_forward", "wdc_dit_forward", "wdc_dit_forward_batch", "wdc_scheduler_step",
-        "wdc_surrogate_step", "wdc_risk_update", "wdc_rollout", "wdc_rollout_batch", "wdc_attn_pad", "wdc_attention", "wdc_linear", "wdc_set_timing",
+        "wdc_surrogate_step", "wdc_surrogate_step_noalloc", "wdc_risk_update", "wdc_rollout", "wdc_rollout_batch", "wdc_attn_pad", "wdc_attention", "wdc_linear", "wdc_set_timing",
         "wdc_timing"]
 
 
@@ -350,6 +351,13 @@ class Context:
     def surrogate_step(self, state: "State", z, k: int, steps: int, zhat) -> dict:
         log = StepLog()
         self._check(self.lib.wdc_surrogate_step(self.h, state.h, _ptr(z), k, steps, _ptr(zhat), C.byref(log)))
+        return log.as_dict()
+
+    def surrogate_step_noalloc(self, state: "State", z, k: int, steps: int, zhat) -> dict:
+        """surrogate_step with the statistics scratch in the library's fixed device array."""
+        log = StepLog()
+        self._check(self.lib.wdc_surrogate_step_noalloc(self.h, state.h, _ptr(z), k, steps, _ptr(zhat),
+                                                        C.byref(log)))
         return log.as_dict()
 
     def risk_update(self, state: "State", phase: int, k: int, steps: int, z_cur=None, z_next=None) -> dict:

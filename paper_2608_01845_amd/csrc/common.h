@@ -225,4 +225,14 @@ hipError_t launch_exact_post(const SegPlan &pl, const PostArgs &a, float *partia
 hipError_t launch_reduce_partials(const SegPlan &pl, const float *partials, int nv, double *out, hipStream_t s);
 hipError_t launch_psi(const float *z, const float *v, float dt, float *zn, int64_t n, hipStream_t s);
 
+// Fixed device scratch of the allocation-free surrogate step (one array per
+// device, held until the process ends): per-block partial sums of the
+// statistics kernels at offset 0, their per-segment float64 reductions at
+// kScratchRedOffset. Sized for the largest plan (16 channels x 8 segments x
+// 64 slices, POST_NV values each).
+constexpr size_t kScratchRedOffset = (size_t)16 * 8 * 64 * POST_NV * sizeof(float);
+constexpr size_t kScratchBytes = kScratchRedOffset + (size_t)16 * 8 * POST_NV * sizeof(double);
+// Device address of that array on the current device, looked up once per device.
+hipError_t scratch_address(void **out);
+
 }  // namespace wdc

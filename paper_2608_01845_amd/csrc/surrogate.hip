@@ -17,6 +17,13 @@
 // rollout reads each latent once per step (Eq. (2), (5), (6)).
 #include "common.h"
 
+#include <mutex>
+
+// Statistics scratch of the allocation-free surrogate step (layout in common.h).
+// Host code must not pass this name to a kernel: it uses the device address
+// that scratch_address() looks up per device.
+static __device__ __align__(256) unsigned char scratch[wdc::kScratchBytes];
+
 namespace wdc {
 
 namespace {
@@ -288,6 +295,26 @@ hipError_t launch_reduce_partials(const SegPlan &pl, const float *partials, int 
   int total = pl.nseg() * nv;
   hipLaunchKernelGGL(k_reduce, dim3((total + 127) / 128), dim3(128), 0, s, partials, pl.nseg(), pl.splits, nv, out);
   return hipGetLastError();
+}
+
+hipError_t scratch_address(void **out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_psi(const float *z, const float *v, float dt, float *zn, int64_t n, hipStream_t s) {

@@ -601,10 +601,19 @@ void summary_tail(const wdc_state *st, double *s) {
   for (int i = 0; i < GCAM; ++i) s[o + 48 + i] = 0.0;  // depth: unavailable
 }
 
-wdc_status fetch(wdc_state *st, int nv) {
+// Device buffers the statistics kernels write: per-block partial sums and
+// their per-segment float64 reductions (the state's own, or the fixed scratch
+// of the allocation-free entry point).
+struct Scratch {
+  float *part;
+  double *red;
+};
+Scratch own_scratch(wdc_state *st) { return Scratch{st->partials, st->d_red}; }
+
+wdc_status fetch(wdc_state *st, int nv, Scratch sc) {
   wdc_ctx *c = st->ctx;
-  HIPCHK(c, launch_reduce_partials(st->plan, st->partials, nv, st->d_red, c->stream));
-  HIPCHK(c, hipMemcpyAsync(st->h_red, st->d_red, sizeof(double) * st->plan.nseg() * nv, hipMemcpyDeviceToHost,
+  HIPCHK(c, launch_reduce_partials(st->plan, sc.part, nv, sc.red, c->stream));
+  HIPCHK(c, hipMemcpyAsync(st->h_red, sc.red, sizeof(double) * st->plan.nseg() * nv, hipMemcpyDeviceToHost,
                            c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   return WDC_OK;
@@ -619,8 +628,9 @@ void log_clear(wdc_step_log *l) {
 
 // Pass 1 + candidate (Eq. (2)-(5)) for step k; keeps it pending in the state.
 // pre: pass-1 statistics of z [nseg, PRE_NV] already at hand, else null (computed here).
+// sc: where the statistics kernels put their partial sums.
 wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zhat, wdc_step_log *log,
-                          const double *pre = nullptr) {
+                          const double *pre, Scratch sc) {
   wdc_ctx *c = st->ctx;
   const auto &p = c->p;
   const int nseg = st->plan.nseg();
@@ -628,8 +638,8 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
   if (!pre) {
     const double bytes = (za ? 8.0 : 4.0) * c->E;
     HIPCHK(c, timed(c, WDC_T_STATS, bytes,
-                    [&] { return launch_stats_pre(st->plan, z, za, st->partials, c->stream); }));
-    CHK(fetch(st, PRE_NV));
+                    [&] { return launch_stats_pre(st->plan, z, za, sc.part, c->stream); }));
+    CHK(fetch(st, PRE_NV, sc));
     pre = st->h_red;
   }
   std::vector<double> sz(nseg), sd(nseg);
@@ -744,8 +754,8 @@ wdc_status surrogate_step(wdc_state *st, const float *z, int k, int S, float *zh
   for (int i : slots) simm = std::min(simm, std::fabs(sims[i] - p.theta_sim));
   const double obytes = (4.0 * m + 4.0 + (za ? 4.0 : 0.0)) * c->E;
   HIPCHK(c, timed(c, WDC_T_OBSERVE, obytes,
-                  [&] { return launch_observe(st->plan, src, coef, m, za, zhat, st->partials, c->stream); }));
-  CHK(fetch(st, OBS_NV));
+                  [&] { return launch_observe(st->plan, src, coef, m, za, zhat, sc.part, c->stream); }));
+  CHK(fetch(st, OBS_NV, sc));
   double nonfinite = 0;
   st->pre_obs.resize((size_t)nseg * PRE_NV);
   for (int i = 0; i < nseg; ++i) {
@@ -826,7 +836,7 @@ wdc_status post_exact(wdc_state *st, const float *z, const float *v, float *zn, 
   const double pbytes = 4.0 * c->E * (2 + a.has_anchor + a.has_zhat + (a.v ? 1 : 0) + 2 + (a.in_slot ? 1 : 0));
   HIPCHK(c, timed(c, WDC_T_EXACT_POST, pbytes,
                   [&] { return launch_exact_post(st->plan, a, st->partials, c->stream); }));
-  CHK(fetch(st, POST_NV));
+  CHK(fetch(st, POST_NV, own_scratch(st)));
   std::vector<double> sn(nseg), sdn(nseg), sdx(nseg);
   double qn = 0, qdn = 0, qdx = 0, acf = 0, an = 0;
   st->pre_post.resize((size_t)nseg * PRE_NV);
@@ -1303,7 +1313,29 @@ wdc_status wdc_scheduler_step(wdc_ctx *ctx, const float *d_z, const float *d_v, 
 wdc_status wdc_surrogate_step(wdc_ctx *ctx, wdc_state *st, const float *d_z, int32_t k, int32_t S, float *d_zhat,
                               wdc_step_log *h_log) {
   if (!ctx || !st || st->ctx != ctx || !d_z || !d_zhat || !h_log || S < 1 || k < 0 || k >= S) return WDC_E_ARG;
-  return surrogate_step(st, d_z, k, S, d_zhat, h_log);
+  return surrogate_step(st, d_z, k, S, d_zhat, h_log, nullptr, own_scratch(st));
+}
+
+wdc_status wdc_surrogate_step_noalloc(wdc_ctx *ctx, wdc_state *st, const float *d_z, int32_t k, int32_t S,
+                                      float *d_zhat, wdc_step_log *h_log) {
+  if (!ctx || !st || st->ctx != ctx || !d_z || !d_zhat || !h_log || S < 1 || k < 0 || k >= S) return WDC_E_ARG;
+  // the statistics kernels write OBS_NV values per block at most (pass 1: PRE_NV)
+  const size_t part = (size_t)st->plan.nblocks() * OBS_NV * sizeof(float);
+  const size_t red = (size_t)st->plan.nseg() * OBS_NV * sizeof(double);
+  if (part > kScratchRedOffset || red > kScratchBytes - kScratchRedOffset) {
+    set_err(ctx, "latent needs %zu + %zu bytes of statistics scratch, more than the fixed %zu + %zu", part, red,
+            kScratchRedOffset, kScratchBytes - kScratchRedOffset);
+    return WDC_E_WORKSPACE;
+  }
+  void *p = nullptr;
+  HIPCHK(ctx, scratch_address(&p));
+  const Scratch sc{(float *)p, (double *)((char *)p + kScratchRedOffset)};
+  // kernel timing records HIP events, which this entry point does not create
+  const bool timing = ctx->timing;
+  ctx->timing = false;
+  const wdc_status s = surrogate_step(st, d_z, k, S, d_zhat, h_log, nullptr, sc);
+  ctx->timing = timing;
+  return s;
 }
 
 wdc_status wdc_risk_update(wdc_ctx *ctx, wdc_state *st, int32_t phase, int32_t k, int32_t S, const float *d_z_cur,
@@ -1387,7 +1419,7 @@ wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, 
     for (int b = 0; b < B; ++b) {
       Sample &q = sm[b];
       wdc_step_log *lg = h_log ? &h_log[(size_t)b * S + k] : &tmp;
-      CHK(surrogate_step(q.st, q.zc, k, S, q.zh, lg, k > 0 ? q.pre.data() : nullptr));
+      CHK(surrogate_step(q.st, q.zc, k, S, q.zh, lg, k > 0 ? q.pre.data() : nullptr, own_scratch(q.st)));
       pre_decision(q.st, k, S, mode, h_forced ? h_forced[(size_t)b * S + k] : 0, lg);
       if (q.st->pend_surrogate) {
         post_surrogate(q.st, lg);
