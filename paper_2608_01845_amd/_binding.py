@@ -260,6 +260,12 @@ class Context:
             seen += 1
         return seen
 
+    def bind_weights(self, blob):
+        """Bind an existing weight blob (a uint8 device tensor, e.g. another context's
+        ``weights`` for the same model) instead of this context's own."""
+        self._check(self.lib.wdc_bind_weights(self.h, C.c_void_p(blob.data_ptr()), blob.numel()))
+        self.weights = blob
+
     def init_random_weights(self, seed: int = 0, std: float = 0.02):
         self._check(self.lib.wdc_init_weights_random(self.h, C.c_void_p(self.weights.data_ptr()),
                                                      self.weights.numel(), seed, std))

@@ -88,7 +88,24 @@ enum Epi {
   EPI_STORE_F32 = 3, // c (float32) = acc + bias
   // EPI_GATE_RES with the float32 stream's read-modify-write marked
   // non-temporal; chosen by launch_gemm, not by callers
-  EPI_GATE_RES_NT = 4
+  EPI_GATE_RES_NT = 4,
+  // fused projection of q, k and v (columns [0, d), [d, 2d), [2d, 3d)): the
+  // bf16 result goes straight into the attention layouts with per-head
+  // RMSNorm and rotary embedding on q and k (GemmArgs::qkv); no c output.
+  // Only where gemm_qkv_fusable() holds.
+  EPI_QKV = 5
+};
+
+// Destination of EPI_QKV. Row r of batch entry z of the product is token
+// row0 + r % rps of sample z + r / rps; q and k of sample b, head h, token j at
+// ((b * heads + h) * n_pad + j) * hd, v transposed at ((b * heads + h) * hd + e)
+// * n_pad + vt(j), vt swapping bits 2 and 3 of j (the key order of the
+// attention kernels' V^T operand).
+struct QkvOut {
+  void *q, *k, *v;
+  const float2 *rope;     // [n_video, hd/2] (cos, sin) or null
+  int64_t n_pad, n_video, rps, row0;
+  int heads, hd, d, qk_norm;
 };
 
 struct GemmArgs {
@@ -107,10 +124,14 @@ struct GemmArgs {
   // block-to-tile order of the MFMA kernels, chosen by launch_gemm: 0 groups
   // of 8 M tiles, 1 one 8 x 4 tile rectangle per XCD per dispatch round
   int order;
+  QkvOut qkv;        // EPI_QKV only
 };
 
 // dtype: 0 float32, 1 bfloat16
 hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s);
+// Whether launch_gemm runs this product (epi EPI_STORE shape) on the 256 x 256
+// kernels, the only ones with the EPI_QKV epilogue.
+bool gemm_qkv_fusable(int dtype, const GemmArgs &g);
 
 // True the first time it is called with this flag array on the current device
 // (kernel attributes such as the dynamic LDS limit are set per device). A

@@ -160,8 +160,11 @@ __device__ __forceinline__ uint4 pack8(const float (&x)[8]) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// (No fused multiply-adds in the norm and rotation arithmetic, here and in the
+// GEMM's fused q/k epilogue, so both give the same bits.)
 template <int HD>
 __global__ __launch_bounds__(256) void k_qk_prep8(QKVPrepArgs a) {
+#pragma clang fp contract(off)
   constexpr int TPH = HD / 8;              // threads per head row
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int c = (int)(gid % TPH);

@@ -151,6 +151,127 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, p);
 }
 
+// ---------------------------------------------------------------- fused q/k/v epilogue (EPI_QKV)
+__device__ __forceinline__ void unpack8(const uint4 &u, float (&x)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack8(const float (&x)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+// V^T position of token j (and token of position j): bits 2 and 3 swapped
+__device__ __forceinline__ int64_t vt_swap(int64_t j) { return (j & ~(int64_t)12) | ((j & 4) << 1) | ((j & 8) >> 1); }
+
+// The block's 256 x 256 bf16 tile (bias added, rounded once) sits in LDS as the
+// staged epilogue leaves it: wave (wm, wn) of 2 x 4 holds rows 128 wm.., columns
+// 64 wn.. as 128-byte rows, 16-byte chunk c of row r at c ^ (r & 7). The tile
+// lies inside the q, k or v columns (d is a multiple of 256).
+__device__ __forceinline__ const char *qkv_chunk(const char *smem, int row, int cc) {
+  const int slice = (row >> 7) * 4 + (cc >> 3), r = row & 127;
+  return smem + slice * (128 * 128) + r * 128 + (((cc & 7) ^ (r & 7)) * 16);
+}
+
+// q or k: per head row the RMSNorm (float32, eps 1e-6) and the rotation of the
+// video tokens' pairs (2p, 2p + 1), one more bf16 rounding, 16-byte stores of
+// whole head rows. HD / 8 consecutive lanes hold one head row. The arithmetic
+// is that of the separate preparation kernel (k_qk_prep8), without fused
+// multiply-adds in either, so both give the same bits.
+template <int HD>
+__device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, int64_t m0, int h0, bf16_t *dst) {
+#pragma clang fp contract(off)
+  const QkvOut &o = g.qkv;
+  constexpr int TPH = HD / 8;
+#pragma unroll 2
+  for (int it = 0; it < 16; ++it) {
+    const int cg = it * 512 + threadIdx.x, row = cg >> 5, cc = cg & 31;
+    const int hh = cc / TPH, c = cc % TPH;
+    const int64_t r = m0 + row;
+    float x[8];
+    unpack8(*(const uint4 *)qkv_chunk(smem, row, cc), x);
+    if (o.qk_norm) {
+      float sq = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sq += x[e] * x[e];
+#pragma unroll
+      for (int off = TPH / 2; off > 0; off >>= 1) sq += __shfl_xor(sq, off, 64);
+      const float rs = rsqrtf(sq / (float)HD + 1e-6f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] *= rs;
+    }
+    if (r >= g.m) continue;
+    const int64_t b = (int64_t)blockIdx.z + r / o.rps, j = o.row0 + r % o.rps;
+    if (o.rope && j < o.n_video) {
+      const float4 *cs4 = (const float4 *)(o.rope + j * (HD / 2) + 4 * c);
+      const float4 c01 = cs4[0], c23 = cs4[1];
+      const float cs[8] = {c01.x, c01.y, c01.z, c01.w, c23.x, c23.y, c23.z, c23.w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const float co = cs[2 * p], si = cs[2 * p + 1];
+        const float t0 = x[2 * p] * co - x[2 * p + 1] * si, t1 = x[2 * p] * si + x[2 * p + 1] * co;
+        x[2 * p] = t0;
+        x[2 * p + 1] = t1;
+      }
+    }
+    *(uint4 *)(dst + ((b * o.heads + h0 + hh) * o.n_pad + j) * HD + 8 * c) = pack8(x);
+  }
+}
+
+// v: transposed into [heads, hd, n_pad] in the V^T key order. A tile whose
+// first token is 16-aligned and whose rows all belong to one sample writes 8
+// consecutive positions (one 16-byte store) per lane for every group of 16
+// tokens it holds whole; partial groups and other tiles go element by element
+// (positions of missing tokens are padding, zeroed separately).
+template <int HD>
+__device__ __forceinline__ void v_scatter(const GemmArgs &g, const char *smem, int64_t m0, int h0) {
+  const QkvOut &o = g.qkv;
+  bf16_t *v = (bf16_t *)o.v;
+  auto at = [&](int row, int col) -> uint32_t {
+    return *(const bf16_t *)(qkv_chunk(smem, row, col >> 3) + 2 * (col & 7));
+  };
+  const int64_t mr = m0 % o.rps;
+  const bool clean = (o.row0 + mr) % 16 == 0 && mr + 256 <= o.rps;
+  if (clean) {
+    const int64_t b = (int64_t)blockIdx.z + m0 / o.rps, j0 = o.row0 + mr;
+#pragma unroll 2
+    for (int it = 0; it < 16; ++it) {
+      const int og = it * 512 + threadIdx.x, col = og >> 5, p8 = og & 31;
+      const int hh = col / HD, e = col % HD, grp = 16 * (p8 >> 1), half = p8 & 1;
+      bf16_t *dst = v + ((b * o.heads + h0 + hh) * HD + e) * o.n_pad + j0;
+      if (m0 + grp + 16 <= g.m) {
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t0 = grp + (int)vt_swap(8 * half + 2 * i), t1 = grp + (int)vt_swap(8 * half + 2 * i + 1);
+          w[i] = at(t0, col) | (at(t1, col) << 16);
+        }
+        *(uint4 *)(dst + 8 * p8) = make_uint4(w[0], w[1], w[2], w[3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int t = grp + (int)vt_swap(8 * half + i);
+          if (m0 + t < g.m) dst[8 * p8 + i] = (bf16_t)at(t, col);
+        }
+      }
+    }
+  } else {
+    for (int it = 0; it < 128; ++it) {
+      const int idx = it * 512 + threadIdx.x, row = idx >> 8, col = idx & 255;
+      const int64_t r = m0 + row;
+      if (r >= g.m) continue;
+      const int64_t b = (int64_t)blockIdx.z + r / o.rps, j = o.row0 + r % o.rps;
+      const int hh = col / HD, e = col % HD;
+      v[((b * o.heads + h0 + hh) * HD + e) * o.n_pad + vt_swap(j)] = (bf16_t)at(row, col);
+    }
+  }
+}
+
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   using C = Cfg<BM, BN, WM, WN>;
@@ -158,7 +279,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   // lane holds 4 consecutive columns of one row (8-byte stores); float32 outputs
   // keep C tiles, whose lanes cover 32 consecutive columns of two rows (a full
   // 128-byte line per read-modify-write instruction)
-  constexpr bool TR = EPI == EPI_STORE || EPI == EPI_GELU;
+  constexpr bool TR = EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_QKV;
+  static_assert(EPI != EPI_QKV || (BM == 256 && BN == 256 && WM == 2 && WN == 4), "EPI_QKV: 256 x 256, 8 waves");
   constexpr bool RES = EPI == EPI_GATE_RES || EPI == EPI_GATE_RES_NT;   // gated residual into the float32 stream
   constexpr bool STAGE_OUT = BM == 256;   // bf16 output through LDS, whole-line non-temporal stores
   const GemmArgs g = batch_entry<bf16_t>(g0);
@@ -415,6 +537,22 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
         }
       }
     }
+    if constexpr (EPI == EPI_QKV) {
+      __syncthreads();                      // every wave's slice is written
+      const int region = (int)(n0 / g.qkv.d), h0 = (int)((n0 % g.qkv.d) / g.qkv.hd);
+      if (region < 2) {
+        bf16_t *dst = (bf16_t *)(region == 0 ? g.qkv.q : g.qkv.k);
+        if (g.qkv.hd == 128)
+          qk_scatter<128>(g, smem, m0, h0, dst);
+        else
+          qk_scatter<64>(g, smem, m0, h0, dst);
+      } else if (g.qkv.hd == 128) {
+        v_scatter<128>(g, smem, m0, h0);
+      } else {
+        v_scatter<64>(g, smem, m0, h0);
+      }
+      return;
+    }
     typedef __attribute__((ext_vector_type(4))) unsigned u32x4_t;
 #pragma unroll
     for (int s = 0; s < WR / RPI; ++s) {
@@ -552,6 +690,13 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
     case EPI_GELU: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GELU>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GATE_RES: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES>), grid, block, C::LDS_BYTES, s, g); break;
     case EPI_GATE_RES_NT: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_GATE_RES_NT>), grid, block, C::LDS_BYTES, s, g); break;
+    case EPI_QKV:
+      if constexpr (BM == 256 && BN == 256 && WM == 2 && WN == 4) {
+        hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_QKV>), grid, block, C::LDS_BYTES, s, g);
+        break;
+      } else {
+        return hipErrorInvalidValue;
+      }
     default: hipLaunchKernelGGL((k_gemm_mfma<BM, BN, WM, WN, EPI_STORE_F32>), grid, block, C::LDS_BYTES, s, g); break;
   }
   return hipGetLastError();
@@ -569,18 +714,35 @@ hipError_t set_lds_limit() {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
     if (e != hipSuccess) return e;
   }
+  if constexpr (BM == 256 && BN == 256 && WM == 2 && WN == 4)
+    return hipFuncSetAttribute((const void *)k_gemm_mfma<BM, BN, WM, WN, EPI_QKV>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
   return hipSuccess;
 }
+
+bool operands_aligned(const GemmArgs &g) {
+  return ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0 &&
+         (uintptr_t)g.c % 16 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.bias % 8 == 0 && (uintptr_t)g.gate % 16 == 0 &&
+         (g.batch <= 1 || (g.a_bs % 8 == 0 && g.c_bs % 4 == 0 && g.gate_bs % 4 == 0));
+}
 }  // namespace
+
+bool gemm_qkv_fusable(int dtype, const GemmArgs &g) {
+  static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
+  const QkvOut &o = g.qkv;
+  return dtype == 1 && variant == 1 && operands_aligned(g) && g.n % 256 == 0 && g.m >= 512 && g.k < 8192 &&
+         (o.hd == 64 || o.hd == 128) && o.d % 256 == 0 && g.n == 3 * (int64_t)o.d && o.rps > 0 &&
+         o.n_pad % 8 == 0 && (uintptr_t)o.q % 16 == 0 && (uintptr_t)o.k % 16 == 0 && (uintptr_t)o.v % 16 == 0 &&
+         (uintptr_t)o.rope % 16 == 0;
+}
 
 hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
   GemmArgs g = g_in;
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
   if (g.epi == EPI_GATE_RES_NT) return hipErrorInvalidValue;   // internal, chosen below
+  if (g.epi == EPI_QKV && !gemm_qkv_fusable(dtype, g)) return hipErrorInvalidValue;
   // the MFMA kernels read 16-byte operand chunks and write 4-column output groups
-  const bool aligned = ((uintptr_t)g.a % 16 == 0) && ((uintptr_t)g.w % 16 == 0) && g.lda % 8 == 0 && g.k % BK == 0 &&
-                       (uintptr_t)g.c % 16 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.bias % 8 == 0 &&
-                       (uintptr_t)g.gate % 16 == 0 && (g.batch <= 1 || (g.a_bs % 8 == 0 && g.c_bs % 4 == 0 && g.gate_bs % 4 == 0));
+  const bool aligned = operands_aligned(g);
   if (dtype == 1 && aligned) {
     static bool seen[64] = {};
     if (first_on_device(seen)) {
@@ -588,6 +750,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
       if (e == hipSuccess) e = set_lds_limit<256, 256, 2, 4>();
       if (e == hipSuccess) e = set_lds_limit<256, 256, 4, 4>();
       if (e == hipSuccess) e = set_lds_limit<128, 128, 2, 2>();
+      if (e == hipSuccess) e = set_lds_limit<128, 64, 2, 2>();
       if (e != hipSuccess) return e;
     }
     // 256 x 256 block tiles: 8 waves of 128 x 64 by default (two per SIMD). With
@@ -612,6 +775,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
     // outputs take the 128 x 128 kernels, which store 8-byte groups)
     const bool c16 = g.epi == EPI_STORE || g.epi == EPI_GELU;
     const bool out16 = !c16 || ((uintptr_t)g.c % 16 == 0 && g.ldc % 8 == 0 && (g.batch <= 1 || g.c_bs % 8 == 0));
+    if (g.epi == EPI_QKV) return launch_mfma<256, 256, 2, 4>(g, s);
     if (g.n % 256 == 0 && g.m >= 512 && out16) {
       // Tail split for a single large long-K product on a 256-CU device: the
       // rows whose 256 x 256 tiles fill whole dispatch rounds (m1 tiles, a
@@ -640,6 +804,8 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
       return big(g);
     }
     if (g.n % 128 == 0) return launch_mfma<128, 128, 2, 2>(g, s);
+    // narrow outputs (the output head: n = 64 latent values per token)
+    if (g.n % 64 == 0) return launch_mfma<128, 64, 2, 2>(g, s);
   }
   dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64), g.batch > 1 ? g.batch : 1), block(256);
   if (dtype == 1)

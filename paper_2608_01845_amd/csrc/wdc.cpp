@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <string>
@@ -56,6 +57,9 @@ struct wdc_ctx {
   float *tok = nullptr;
   float2 *rope = nullptr;
   float *r_v = nullptr;  // [mb, E] velocities of a batched forward inside a rollout
+  // q/k/v preparation in the projection's epilogue where the GEMM allows it
+  // (WDC_FUSE_QKV=0: always the separate kernels, for comparison)
+  bool fuse_qkv = true;
   // timing
   bool timing = false;
   std::vector<TimedEvent> events;
@@ -363,6 +367,55 @@ wdc_status qkv_prep(wdc_ctx *c, const void *src, int64_t ld, int64_t row0, int64
   return WDC_OK;
 }
 
+// q/k/v projection of the modulated rows [row0, row0 + rows) of every sample
+// (a: the first of them, row stride D). batched: one batch entry per sample
+// (sample stride N rows); else one product over all samples' rows (row0 = 0,
+// rows = N). The 256 x 256 GEMM writes q, k and v^T straight into the
+// attention layouts (per-head RMSNorm and RoPE in its epilogue); products it
+// does not run (few rows) take the plain GEMM into the qkv buffer and the
+// separate preparation kernels, with the same arithmetic.
+wdc_status qkv_project(wdc_ctx *c, const void *a, const void *w, const void *bias, int64_t row0, int64_t rows,
+                       bool batched) {
+  const int64_t D = c->D, N = c->n, NB = c->nb;
+  if (!w) {
+    set_err(c, "weights not bound");
+    return WDC_E_WORKSPACE;
+  }
+  GemmArgs g{};
+  g.a = a;
+  g.w = w;
+  g.bias = bias;
+  g.lda = D;
+  g.ldc = 3 * D;
+  g.m = batched ? rows : NB * rows;
+  g.n = 3 * D;
+  g.k = D;
+  g.epi = EPI_QKV;
+  g.batch = batched ? (int)NB : 1;
+  g.a_bs = batched ? N * D : 0;
+  QkvOut &o = g.qkv;
+  o.q = c->q;
+  o.k = c->k;
+  o.v = c->v;
+  o.rope = (c->d.rope_t + c->d.rope_h + c->d.rope_w) ? c->rope : nullptr;
+  o.n_pad = c->n_pad;
+  o.n_video = c->nv;
+  o.rps = batched ? rows : N;
+  o.row0 = row0;
+  o.heads = c->H;
+  o.hd = c->hd;
+  o.d = (int)D;
+  o.qk_norm = c->d.qk_norm;
+  if (c->fuse_qkv && gemm_qkv_fusable(c->d.dtype, g)) {
+    HIPCHK(c, timed(c, WDC_T_GEMM, 2.0 * g.m * g.n * g.k * g.batch, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
+    return WDC_OK;
+  }
+  void *out = elem(c, c->qkv, row0 * 3 * D);
+  CHK(gemm(c, a, D, w, bias, out, 3 * D, g.m, 3 * D, D, EPI_STORE, nullptr,
+           batched ? Batch{(int)NB, N * D, N * 3 * D, 0} : Batch()));
+  return qkv_prep(c, out, 3 * D, row0, rows);
+}
+
 // LayerNorm + modulation of rows [row0, row0 + rows) of every sample, with the
 // shift/scale vectors of sample 0 given (the others follow at mod_stride)
 wdc_status ln_mod(wdc_ctx *c, int64_t row0, int64_t rows, const float *shift, const float *scale) {
@@ -389,8 +442,7 @@ wdc_status seq_block(wdc_ctx *c, int i) {
   const Batch gr{(int)NB, N * LC, N * D, MS};
   CHK(mod_gemv(c, pre + ".ada", 0));
   CHK(ln_mod(c, 0, N, m, m + D));
-  CHK(gemm(c, c->h, D, W(c, pre + ".qkv.w"), W(c, pre + ".qkv.b"), c->qkv, 3 * D, NB * N, 3 * D, D, EPI_STORE));
-  CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
+  CHK(qkv_project(c, c->h, W(c, pre + ".qkv.w"), W(c, pre + ".qkv.b"), 0, N, false));
   CHK(attention(c, c->cat, LC));
   CHK(gemm(c, c->cat, LC, W(c, pre + ".out.w"), W(c, pre + ".out.b"), c->x, D, N, D, D, EPI_GATE_RES, m + 2 * D, gr));
   CHK(ln_mod(c, 0, N, m + 3 * D, m + 4 * D));
@@ -415,10 +467,8 @@ wdc_status dual_block(wdc_ctx *c, int i) {
   for (auto &s : st) {
     std::string p = pre + "." + s.s;
     CHK(ln_mod(c, s.r0, s.rows, s.m, s.m + D));
-    CHK(gemm(c, elem(c, c->h, s.r0 * D), D, W(c, p + ".qkv.w"), W(c, p + ".qkv.b"), elem(c, c->qkv, s.r0 * 3 * D),
-             3 * D, s.rows, 3 * D, D, EPI_STORE, nullptr, Batch{(int)NB, N * D, N * 3 * D, 0}));
+    CHK(qkv_project(c, elem(c, c->h, s.r0 * D), W(c, p + ".qkv.w"), W(c, p + ".qkv.b"), s.r0, s.rows, true));
   }
-  CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
   CHK(attention(c, c->cat, LC));
   for (auto &s : st) {
     std::string p = pre + "." + s.s;
@@ -444,10 +494,9 @@ wdc_status single_block(wdc_ctx *c, int i) {
     set_err(c, "weights not bound");
     return WDC_E_WORKSPACE;
   }
-  CHK(gemm(c, c->h, D, w1, b1, c->qkv, 3 * D, NB * N, 3 * D, D, EPI_STORE));
+  CHK(qkv_project(c, c->h, w1, b1, 0, N, false));
   CHK(gemm(c, c->h, D, w1 + 3 * D * D * c->esz, b1 + 3 * D * c->esz, elem(c, c->cat, D), LC, NB * N, F, D,
            EPI_GELU));
-  CHK(qkv_prep(c, c->qkv, 3 * D, 0, N));
   CHK(attention(c, c->cat, LC));
   CHK(gemm(c, c->cat, LC, W(c, pre + ".lin2.w"), W(c, pre + ".lin2.b"), c->x, D, N, D, LC, EPI_GATE_RES, m + 2 * D,
            Batch{(int)NB, N * LC, N * D, MS}));
@@ -1061,6 +1110,7 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
     return WDC_E_ARG;
   }
   c->mb = d.max_batch > 1 ? d.max_batch : 1;
+  c->fuse_qkv = !(getenv("WDC_FUSE_QKV") && atoi(getenv("WDC_FUSE_QKV")) == 0);
   c->stream = (hipStream_t)stream;
   c->esz = d.dtype == WDC_BF16 ? 2 : 4;
   c->D = d.hidden;

@@ -25,6 +25,15 @@ def rel_l2(a, b) -> float:
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
 
 
+def row_rel_l2(a, b) -> float:
+    """Largest relative L2 error of one row (last axis) over all rows."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    num = np.linalg.norm(a - b, axis=-1)
+    den = np.maximum(np.linalg.norm(b, axis=-1), 1e-30)
+    return float(np.max(num / den))
+
+
 def small_cfg(dtype="bf16", head_dim=64, **kw):
     """A small joint-sequence model with all three block kinds, text tokens and a camera vector."""
     heads = 256 // head_dim

@@ -1,0 +1,66 @@
+"""Run-to-run reproducibility of the HIP path (GPU): the same call twice in one
+process gives bit-identical results. Reductions combine partial sums in a
+fixed order and no kernel uses atomics, so nothing may differ between runs."""
+import numpy as np
+import pytest
+
+import synth
+from tests.gpu_util import context, dev_inputs, small_cfg, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _logs_equal(a, b):
+    assert len(a) == len(b)
+    for x, y in zip(a, b):
+        for key in x:
+            assert np.array_equal(np.asarray(x[key], dtype=np.float64), np.asarray(y[key], dtype=np.float64),
+                                  equal_nan=True), key
+
+
+def test_risk_rollout_twice_is_bitwise_identical():
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config("tiny")
+    ctx = context(cfg, params=wdc.default_params(tau_risk=0.2))
+    _, dv = dev_inputs(ctx, cfg)
+    out = []
+    for _ in range(2):
+        z = dv["z_T"].clone()
+        sched, logs = ctx.rollout(ctx.new_state(), z, 8, dv["cond"], mode=wdc.MODE_RISK)
+        out.append((z, sched, logs))
+    assert 0 < sum(out[0][1]) < 8              # both branches ran
+    assert torch.equal(out[0][0], out[1][0]) and out[0][1] == out[1][1]
+    _logs_equal(out[0][2], out[1][2])
+
+
+@pytest.mark.parametrize("name", ["small", "mid"])
+def test_bf16_forward_twice_is_bitwise_identical(name):
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = small_cfg("bf16") if name == "small" else synth.get_config("mid")
+    ctx = wdc.Context(cfg)
+    ctx.init_random_weights(seed=5, std=0.02)
+    _, dv = dev_inputs(ctx, cfg)
+    v1 = ctx.forward(dv["z_T"], 0.6, dv["cond"], dv["text"], dv["cam"])
+    v2 = ctx.forward(dv["z_T"], 0.6, dv["cond"], dv["text"], dv["cam"])
+    assert torch.isfinite(v1).all() and float(v1.abs().max()) > 0
+    assert torch.equal(v1, v2)
+
+
+def test_replay_rollout_on_unaligned_latent_twice_is_bitwise_identical():
+    """The 5B latent (segment starts not 16-byte aligned), recorded velocities."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config("5b")
+    steps = 12
+    ctx = wdc.Context(cfg, allocate_weights=False, params=wdc.default_params(tau_risk=0.3))
+    vel = torch.from_numpy(synth.gen_replay_velocities(cfg, steps)).cuda()
+    z0 = torch.from_numpy(synth.gen_inputs(cfg)["z_T"]).cuda()
+    out = []
+    for _ in range(2):
+        z = z0.clone()
+        sched, logs = ctx.rollout(ctx.new_state(), z, steps, mode=wdc.MODE_RISK, replay_v=vel)
+        out.append((z, sched, logs))
+    assert torch.equal(out[0][0], out[1][0]) and out[0][1] == out[1][1]
+    _logs_equal(out[0][2], out[1][2])
