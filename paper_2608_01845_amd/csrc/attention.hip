@@ -232,6 +232,7 @@ __device__ __forceinline__ void pp_wait4(int n_outstanding) {
 // rescaled and P recomputed). Any reference gives the same normalised result,
 // and P <= 2^64 keeps O and l far from float overflow.
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 constexpr float PPR_LIMIT = 0x1p64f;
 
 // accumulator tile that starts a row's Q K contraction at -m
@@ -674,12 +675,27 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
         WDC_PPR3_READ(q_ + 4, vb_, kb_)                                                          \
       else  /* the next step's first reads: V^T of tile t + 1, published by the last barrier */  \
         WDC_PPR3_READ(q_ + 4 - NMF, vn_, kb_)                                                    \
-      _Pragma("unroll") for (int x_ = 0; x_ < EPM; ++x_) {                                       \
-        const int ei_ = q_ * EPM + x_, kt_ = ei_ / 16, e_ = ei_ % 16;                            \
-        pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);         \
-        if (ei_ & 1)                                                                             \
-          ls = __builtin_amdgcn_fdot2_f32_bf16(                                                  \
-              bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false);\
+      if constexpr (EPM == 2) {                                                                  \
+        /* both exponentials of a pair, converted together; the empty asm pins */                \
+        /* the pair under this MFMA (left free, the compiler sinks all of them */                \
+        /* past the stream, where they no longer overlap the matrix cores) */                    \
+        const int ei_ = 2 * q_, kt_ = ei_ / 16, e_ = ei_ % 16;                                   \
+        const bf16x2_t pr_ = {(__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]),                     \
+                              (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_ + 1])};                \
+        uint32_t u_ = __builtin_bit_cast(uint32_t, pr_);                                         \
+        asm volatile("" : "+v"(u_));                                                             \
+        u32x4_t w_ = __builtin_bit_cast(u32x4_t, pf[c][2 * kt_ + e_ / 8]);                        \
+        w_[(e_ % 8) / 2] = u_;                                                                   \
+        pf[c][2 * kt_ + e_ / 8] = __builtin_bit_cast(bf16x8, w_);                                \
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u_), one2_, ls, false); \
+      } else {                                                                                   \
+        _Pragma("unroll") for (int x_ = 0; x_ < EPM; ++x_) {                                     \
+          const int ei_ = q_ * EPM + x_, kt_ = ei_ / 16, e_ = ei_ % 16;                          \
+          pf[c][2 * kt_ + e_ / 8][e_ % 8] = (__bf16)__builtin_amdgcn_exp2f(S[c][kt_][e_]);       \
+          if (ei_ & 1)                                                                           \
+            ls = __builtin_amdgcn_fdot2_f32_bf16(                                                \
+                bf16x2_t{pf[c][2 * kt_ + e_ / 8][(e_ - 1) % 8], pf[c][2 * kt_ + e_ / 8][e_ % 8]}, one2_, ls, false);\
+        }                                                                                        \
       }                                                                                          \
       __builtin_amdgcn_sched_barrier(0);                                                         \
     }                                                                                            \

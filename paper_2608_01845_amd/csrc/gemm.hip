@@ -188,7 +188,8 @@ __device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, 
 #pragma clang fp contract(off)
   const QkvOut &o = g.qkv;
   constexpr int TPH = HD / 8;
-#pragma unroll 2
+  // (unrolled by 4: the rotation table loads of four rows are in flight together)
+#pragma unroll 4
   for (int it = 0; it < 16; ++it) {
     const int cg = it * 512 + threadIdx.x, row = cg >> 5, cc = cg & 31;
     const int hh = cc / TPH, c = cc % TPH;
@@ -237,11 +238,16 @@ __device__ __forceinline__ void v_scatter(const GemmArgs &g, const char *smem, i
   };
   const int64_t mr = m0 % o.rps;
   const bool clean = (o.row0 + mr) % 16 == 0 && mr + 256 <= o.rps;
+  static_assert(HD == 64 || HD == 128, "head size");
   if (clean) {
+    // a wavefront's lanes take 64 consecutive columns at one chunk of 8
+    // positions: every LDS read of the wave hits one 128-byte tile row segment
+    // (columns of a fixed token are contiguous; tokens of a fixed column 16
+    // apart would all fall on one bank)
     const int64_t b = (int64_t)blockIdx.z + m0 / o.rps, j0 = o.row0 + mr;
 #pragma unroll 2
     for (int it = 0; it < 16; ++it) {
-      const int og = it * 512 + threadIdx.x, col = og >> 5, p8 = og & 31;
+      const int col = threadIdx.x & 255, p8 = 2 * it + (threadIdx.x >> 8);
       const int hh = col / HD, e = col % HD, grp = 16 * (p8 >> 1), half = p8 & 1;
       bf16_t *dst = v + ((b * o.heads + h0 + hh) * HD + e) * o.n_pad + j0;
       if (m0 + grp + 16 <= g.m) {

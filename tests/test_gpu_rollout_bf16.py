@@ -22,6 +22,9 @@ from tests.gpu_util import TOL_BF16_FINAL, rel_l2, small_cfg, torch_cuda
 pytestmark = pytest.mark.gpu
 
 MIN_MARGIN = 0.03
+# the mid sweep's thresholds (stored oracle rollouts) keep every R_cand at least
+# 1.2% away: twenty times the drift measured on the small model
+MIN_MARGIN_MID = 0.01
 
 
 def _rel(a, b):
@@ -72,3 +75,48 @@ def test_small_bf16_rollout_threshold_sweep():
         assert sched == ref.schedule
         assert err <= TOL_BF16_FINAL
 
+
+def test_mid_bf16_rollout_threshold_sweep():
+    """The mid workload (8 blocks, D = 1024, 16 x 64 heads, 2,688 tokens, bf16),
+    20 steps, thresholds giving 0, 2, ..., 12 surrogate steps (0-60% skipped).
+    The oracle's rollouts (tests/golden/make_tau_sweeps.py) are stored: per
+    threshold its schedule, controller log, the final latent at 2,048 fixed
+    positions and the final latent's norm."""
+    import json
+    import os
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "mid_tau_sweep.json")
+    gold = json.load(open(path))
+    cfg = synth.get_config("mid")
+    S = gold["steps"]
+    assert gold["workload"] == "mid" and S == 20
+    idx = torch.tensor(gold["sample_index"], device="cuda")
+    counts = sorted(sum(case["schedule"]) for case in gold["cases"])
+    assert counts == list(range(0, 13, 2))
+    base = wdc.Context(cfg)
+    base.load_weights(synth.gen_weights(cfg))
+    inp = synth.gen_inputs(cfg)
+    cond = base.to_device(inp["cond"])
+    for case in gold["cases"]:
+        tau = case["tau"]
+        assert case["margin"] >= MIN_MARGIN_MID
+        ctx = wdc.Context(cfg, params=wdc.default_params(tau_risk=tau), allocate_weights=False)
+        ctx.bind_weights(base.weights)
+        z = torch.from_numpy(inp["z_T"]).cuda()
+        sched, logs = ctx.rollout(ctx.new_state(), z, S, cond, mode=wdc.MODE_RISK)
+        got = z.reshape(-1)[idx].double().cpu().numpy()
+        ref = np.asarray(case["final_samples"])
+        err = rel_l2(got, ref)
+        norm_err = abs(float(z.double().norm()) - case["final_norm"]) / case["final_norm"]
+        drift = 0.0
+        for g, o in zip(logs, case["log"]):
+            assert g["exact"] == int(o["exact"]) and g["bank"] == int(o["bank"]) and g["support"] == int(o["support"])
+            assert g["available"] == int(o["available"]) and g["finite"] == int(o["finite"])
+            for key in ("d_z", "p", "r_cand", "eta", "R"):
+                drift = max(drift, _rel(g[key], o[key]))
+        print(f"{sum(sched)} surrogate steps: tau {tau:.5g} margin {case['margin']:.3f} sampled final rel_l2 "
+              f"{err:.2e}, norm {norm_err:.2e}, log drift {drift:.2e}")
+        assert sched == case["schedule"]
+        assert err <= TOL_BF16_FINAL and norm_err <= TOL_BF16_FINAL
+        del ctx
