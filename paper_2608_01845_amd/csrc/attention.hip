@@ -13,14 +13,11 @@
 //    8 accumulator values a lane holds for 16 consecutive keys become its 8
 //    bf16 k-values, and the V^T operand is read with the same key order, so P
 //    never goes through LDS;
-//  * softmax in base 2 against a per-row reference max (k_attn_bf16_ppr3, the
-//    default, whose step runs the vector work of tile t + 1 inside the MFMA
-//    stream of tiles t and t + 2; k_attn_bf16_ppr, the two-phase form, kept
-//    for comparison).
+//  * softmax in base 2 against a per-row reference max, each step running the
+//    vector work of tile t + 1 inside the MFMA stream of tiles t and t + 2
+//    (k_attn_bf16_ppr3).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
-
-#include <cstdlib>
 
 namespace wdc {
 
@@ -144,72 +141,6 @@ struct TileLoad {
   }
 };
 
-// V^T fragment f (k-step j = f / (HD/32), O tile i = f % (HD/32)) of a tile
-template <int HD>
-__device__ __forceinline__ bf16x8 pp_vfrag(const char *v, const int (&vro)[4], int f) {
-  return *(const bf16x8 *)(v + (f % (HD / 32)) * 32 * KV * 2 + vro[f / (HD / 32)]);
-}
-
-// O^T += V^T P^T for one tile: fragments 0-3 come read (in the previous
-// step), the others are read right before their MFMAs.
-template <int HD>
-__device__ __forceinline__ void pp_pv(f32x16 (&o)[HD / 32], const char *v, const bf16x8 (&pf)[4],
-                                      const int (&vro)[4], const bf16x8 (&pre)[4]) {
-#pragma unroll
-  for (int f = 0; f < 4 * (HD / 32); ++f) {
-    const bf16x8 vf = f < 4 ? pre[f < 4 ? f : 0] : pp_vfrag<HD>(v, vro, f);
-    o[f % (HD / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[f / (HD / 32)], o[f % (HD / 32)], 0, 0, 0);
-  }
-}
-
-// Reference-max kernel (ppr), the two-phase form. 8 wavefronts per block (two
-// per SIMD), 32 queries each, K/V tiles of 64 keys in four K and four V^T LDS
-// buffers. Every tile step of a wave is a matrix phase (O += V^T P^T for tile t,
-// S' for tile t+1, LDS fragment reads scheduled four ahead of the MFMAs)
-// followed by a vector phase (softmax of tile t+1); a step ends with the only
-// block barrier of the step. Within a step the waves run free, so the two waves
-// of a SIMD drift apart and one's vector phase overlaps the other's MFMAs (a
-// ping-pong with a barrier between the phases was 4.6% slower at hd 128 and 11%
-// at hd 64 on the same box).
-// Pipeline (hd 128; hd 64 differs as PprShape below states): group A (waves
-// 0-3) issues the loads of K_{t+3} and V_{t+3} in step t and at the end of step
-// t waits only for the loads of step t-1 (a partial vmcnt), so a tile load has
-// at least two full steps to land. The first four
-// V^T fragment reads of step t+1 go out right after step t's matrix phase
-// (V_{t+1} was published by the barrier that ended step t-1) and land during
-// its vector phase. The step loop is unrolled by four so every LDS fragment
-// address is a per-lane register plus an immediate offset. Buffer reuse: step
-// t reads V_t and K_{t+1}; K_{t+3} overwrites K_{t-1}, last read in step t-2,
-// and V_{t+3} overwrites V_{t-1}, last read in step t-1; before the barrier
-// that ends a step each wave waits for all its LDS reads but the four early
-// ones, whose slot no load of the next step writes.
-// Buffering of the two-phase kernel. hd 128: four K and four V^T slots (128 KB),
-// tiles loaded three steps ahead, a barrier after every step. hd 64 (8 KB
-// tiles): eight slots, tiles loaded six steps ahead and a barrier after every
-// second step, which halves the fixed per-step cost of the short hd 64 step.
-// Slot reuse at hd 64: the load in step t overwrites tile t - 2, whose last
-// reads (V in step t - 2, K in step t - 3) precede the barrier before step t;
-// the barrier after step b waits for the loads of steps up to b - 2, so the
-// tiles step t reads (K_{t+1} and V_t, loaded in steps t - 5 and t - 6) and the
-// early V^T reads are published in time.
-template <int HD> struct PprShape;
-template <> struct PprShape<128> { static constexpr int NB = 4, LEAD = 3, BSTEP = 1; };
-template <> struct PprShape<64> { static constexpr int NB = 8, LEAD = 6, BSTEP = 2; };
-
-// vmcnt wait leaving n of this wave's tile loads in flight (n: loads of the
-// last one or two steps)
-template <int HD>
-__device__ __forceinline__ void ppr_vm_wait(int n) {
-  constexpr int S1 = TileLoad<HD>::K_STRIPES + TileLoad<HD>::V_STRIPES;
-  static_assert(PprShape<HD>::BSTEP * S1 < 16, "vmcnt immediate");
-  if (PprShape<HD>::BSTEP == 2 && n == 2 * S1)
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | ((2 * S1) & 15));
-  else if (n == S1)
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0 | S1);
-  else
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-}
-
 template <int HD>
 __device__ __forceinline__ void pp_wait4(int n_outstanding) {
   constexpr int KS = TileLoad<HD>::K_STRIPES, VS = TileLoad<HD>::V_STRIPES;
@@ -278,220 +209,10 @@ __device__ __forceinline__ float ppr_exp(const f32x16 (&S)[2], bf16x8 (&pf)[4]) 
   return ls;
 }
 
-// vector phase: keys >= valid masked, P = exp2(S'), l += sum P; a lane sum
-// above the limit moves the rows to their true max first
-template <int HD>
-__device__ __forceinline__ void ppr_softmax(f32x16 (&S)[2], bf16x8 (&pf)[4], f32x16 (&o)[HD / 32], float &m,
-                                            f32x16 &mi, float &l, int valid, int lg) {
-  if (valid < KV) {                        // partial last tile only: a branch, not selects
-    asm volatile("" ::: "memory");
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= valid) S[kt][e] = -1e30f;
-  }
-  float ls = ppr_exp(S, pf);
-  if (__any(ls > PPR_LIMIT)) {
-    const float mx = ppr_rowmax(S);
-    const float mn = m + (mx > 8.f ? mx : 0.f);
-    mi = ppr_mtile(mn);
-    const float d = mn - m, alpha = __builtin_amdgcn_exp2f(-d);
-    m = mn;
-    l *= alpha;
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[i][e] *= alpha;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) S[kt][e] -= d;
-    ls = ppr_exp(S, pf);
-  }
-  l += ls;
-}
-
-template <int HD>
-__global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr(AttnArgs a) {
-  constexpr int QB = 256;                  // 8 waves x 32 queries
-  constexpr int NB = PprShape<HD>::NB;     // K buffers and V^T buffers
-  constexpr int LEAD = PprShape<HD>::LEAD; // tiles between a load and its step
-  constexpr int BSTEP = PprShape<HD>::BSTEP;   // tile steps per block barrier
-  constexpr int K_BYTES = KV * HD * 2;
-  constexpr int V_BASE = NB * K_BYTES;     // V^T buffers follow the K buffers
-  using TL = TileLoad<HD>;
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-
-  int h = blockIdx.y, qb = blockIdx.x;
-  if (a.xcd_order) {
-    const int id = blockIdx.x + blockIdx.y * gridDim.x;
-    const int li = id >> 3;
-    h = (id & 7) + 8 * (li / gridDim.x);
-    qb = li % gridDim.x;
-  }
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool grp_a = wid < 4;
-  const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qbase = (int64_t)qb * QB + wid * 32;
-  const bf16_t *Q = (const bf16_t *)a.q + (int64_t)h * a.n_pad * HD;
-
-  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
-  bf16x8 qf[HD / 16];                      // Q^T scaled by sc: scores in log2 units
-#pragma unroll
-  for (int s = 0; s < HD / 16; ++s) {
-    const bf16x8 raw = *(const bf16x8 *)(Q + (qbase + lr) * HD + 16 * s + 8 * lg);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) qf[s][j] = (__bf16)((float)raw[j] * sc);
-  }
-
-  const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
-  const int lw = wid & 3;
-  const TileLoad<HD> tl(lw, lane, a.n_pad);
-  int kro[HD / 16];
-#pragma unroll
-  for (int s = 0; s < HD / 16; ++s) kro[s] = kswz<HD>(lr, 2 * s + lg);
-  int vro[4];                              // V^T fragment offsets, V region base folded in
-#pragma unroll
-  for (int j = 0; j < 4; ++j) vro[j] = V_BASE + vslot(lr, 2 * j + lg);
-
-  const int ntiles = (int)((a.n + KV - 1) / KV);
-  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
-  auto load_k = [&](int b, int tile) {
-#pragma unroll
-    for (int i = 0; i < TL::K_STRIPES; ++i)
-      lds_load16(kdesc, smem + b * K_BYTES + lw * 1024 + i * 4096, tl.kvo, tile * KV * HD * 2 + i * 4096);
-  };
-  auto load_v = [&](int b, int tile) {
-#pragma unroll
-    for (int i = 0; i < TL::V_STRIPES; ++i)
-      lds_load16(vdesc, smem + V_BASE + b * K_BYTES + lw * 1024 + i * 4096, tl.vvo,
-                 tile * KV * 2 + i * 32 * (int)a.n_pad * 2);
-  };
-
-  if (grp_a) {
-#pragma unroll
-    for (int j = 0; j < LEAD; ++j)
-      if (j < ntiles) {
-        load_k(j, j);
-        load_v(j, j);
-      }
-    __builtin_amdgcn_s_waitcnt(WAIT_VM0);
-  }
-  __syncthreads();
-
-  f32x16 o[HD / 32];
-#pragma unroll
-  for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
-  float m = 0.f, l = 0.f;
-  f32x16 mi = ppr_mtile(m);
-  f32x16 S[2];
-  bf16x8 pf[4];
-  ppr_qk<HD>(S, smem, qf, kro, mi);
-  {                                        // m = the first tile's row max
-    const int v0 = ntiles == 1 ? last_valid : KV;
-    if (v0 < KV) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (32 * kt + 8 * (e / 4) + 4 * lg + (e % 4) >= v0) S[kt][e] = -1e30f;
-    }
-    m = ppr_rowmax(S);
-    mi = ppr_mtile(m);
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) S[kt][e] -= m;
-    l = ppr_exp(S, pf);
-  }
-
-  constexpr int NMF = 4 * (HD / 32) + 2 * (HD / 16);   // fragment reads per matrix phase
-  bf16x8 pre[4];                           // first four V^T fragments of the next P V
-  int iss_prev = 0;                        // loads issued in the step before (no barrier after it)
-#pragma unroll
-  for (int f = 0; f < 4; ++f) pre[f] = pp_vfrag<HD>(smem, vro, f);
-  // One tile step with compile-time buffer slot P = t % NB.
-#define WDC_PPR_STEP(P)                                                                          \
-  {                                                                                              \
-    const int t = t0 + (P);                                                                      \
-    int issued = 0;                                                                              \
-    if (grp_a && t + LEAD < ntiles) {                                                            \
-      load_k(((P) + LEAD) % NB, t + LEAD);                                                       \
-      load_v(((P) + LEAD) % NB, t + LEAD);                                                       \
-      issued = TL::K_STRIPES + TL::V_STRIPES;                                                    \
-    }                                                                                            \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-    pp_pv<HD>(o, smem + (P) * K_BYTES, pf, vro, pre);                                            \
-    ppr_qk<HD>(S, smem + (((P) + 1) % NB) * K_BYTES, qf, kro, mi);                               \
-    _Pragma("unroll") for (int i_ = 0; i_ < NMF - 4; ++i_) {                                     \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                         \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                         \
-    }                                                                                            \
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                                           \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-    /* the next P V's first fragments (V^T of tile t + 1, published by the last */               \
-    /* barrier) land during the vector phase */                                                  \
-    _Pragma("unroll") for (int f_ = 0; f_ < 4; ++f_)                                             \
-      pre[f_] = pp_vfrag<HD>(smem + (((P) + 1) % NB) * K_BYTES, vro, f_);                        \
-    __builtin_amdgcn_sched_barrier(0);                                                           \
-    if (t + 1 < ntiles) ppr_softmax<HD>(S, pf, o, m, mi, l, t + 2 < ntiles ? KV : last_valid, lg);\
-    if ((P) % BSTEP == BSTEP - 1) {                                                              \
-      /* only the loads of the last BSTEP steps may still be in flight; every                    \
-         older read is done, and the four just issued read a slot no load of                     \
-         the next LEAD - 1 steps writes */                                                       \
-      if (grp_a) ppr_vm_wait<HD>(iss_prev + issued);                                             \
-      asm volatile("s_waitcnt lgkmcnt(4)\n\ts_barrier" ::: "memory");                            \
-      iss_prev = 0;                                                                              \
-    } else {                                                                                     \
-      iss_prev = issued;                                                                         \
-    }                                                                                            \
-  }
-  for (int t0 = 0; t0 < ntiles; t0 += NB) {
-    WDC_PPR_STEP(0)
-    if (t0 + 1 >= ntiles) break;
-    WDC_PPR_STEP(1)
-    if (t0 + 2 >= ntiles) break;
-    WDC_PPR_STEP(2)
-    if (t0 + 3 >= ntiles) break;
-    WDC_PPR_STEP(3)
-    if constexpr (NB == 8) {
-      if (t0 + 4 >= ntiles) break;
-      WDC_PPR_STEP(4)
-      if (t0 + 5 >= ntiles) break;
-      WDC_PPR_STEP(5)
-      if (t0 + 6 >= ntiles) break;
-      WDC_PPR_STEP(6)
-      if (t0 + 7 >= ntiles) break;
-      WDC_PPR_STEP(7)
-    }
-  }
-#undef WDC_PPR_STEP
-
-  const float lt = l + __shfl_xor(l, 32, 64);
-  const float inv = 1.f / lt;
-  const int64_t q = qbase + lr;
-  if (q < a.n) {
-    bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD);
-#pragma unroll
-    for (int i = 0; i < HD / 32; ++i)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d0 = 32 * i + 8 * g4 + 4 * lg;
-        uint32_t w0 = (uint32_t)f2bf(o[i][4 * g4 + 0] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 1] * inv) << 16);
-        uint32_t w1 = (uint32_t)f2bf(o[i][4 * g4 + 2] * inv) | ((uint32_t)f2bf(o[i][4 * g4 + 3] * inv) << 16);
-        *(uint2 *)(O + d0) = make_uint2(w0, w1);
-      }
-  }
-}
-
-// Three-stage form of the reference-max kernel: step t runs the P V MFMAs of
+// bf16 flash attention. 8 wavefronts per block (two per SIMD), 32 queries each
+// (256 per block); K tiles of 64 keys and V^T tiles reach four K and four V^T
+// LDS slots by direct buffer loads issued by waves 0-3; one block barrier per
+// tile step. Step t runs the P V MFMAs of
 // tile t and the Q K MFMAs of tile t + 2 with the vector phase of tile t + 1
 // (P = exp2(S'), its bf16 conversion and row sum) interleaved into the same
 // instruction stream, so a wave's VALU work executes under its own MFMAs
@@ -766,37 +487,17 @@ hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int HD>
-hipError_t launch_bf16_ppr(const AttnArgs &a, hipStream_t s) {
-  constexpr int LDS = 2 * PprShape<HD>::NB * KV * HD * 2;   // K tiles and V^T tiles
-  static bool seen[64] = {};
-  if (first_on_device(seen)) {
-    const hipError_t e = hipFuncSetAttribute((const void *)k_attn_bf16_ppr<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
-    if (e != hipSuccess) return e;
-  }
-  dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16_ppr<HD>), grid, dim3(512), LDS, s, a);
-  return hipGetLastError();
-}
-
-
-
 }  // namespace
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;
   if (a.n_pad != attn_pad(a.n)) return hipErrorInvalidValue;
   if (dtype == 1) {
-    // Default: the 8-wave reference-max kernel in its three-stage form (ppr3:
-    // 3.5-4.5% faster than the two-phase ppr at the 13B shape, about 2.5% at
-    // hd 64). WDC_ATTN_VARIANT=4 selects the two-phase ppr, for comparison.
-    static const int variant = getenv("WDC_ATTN_VARIANT") ? atoi(getenv("WDC_ATTN_VARIANT")) : 5;
-    static const int xcd = getenv("WDC_ATTN_XCD") ? atoi(getenv("WDC_ATTN_XCD")) : 1;
+    // heads grouped per XCD when the head count allows it (every real workload)
     AttnArgs b = a;
-    b.xcd_order = (xcd && a.heads % 8 == 0) ? 1 : 0;
-    if (a.hd == 128)
-      return variant == 4 ? launch_bf16_ppr<128>(b, s) : launch_bf16_ppr3<128>(b, s);
-    if (a.hd == 64) return variant == 4 ? launch_bf16_ppr<64>(b, s) : launch_bf16_ppr3<64>(b, s);
+    b.xcd_order = a.heads % 8 == 0 ? 1 : 0;
+    if (a.hd == 128) return launch_bf16_ppr3<128>(b, s);
+    if (a.hd == 64) return launch_bf16_ppr3<64>(b, s);
     return hipErrorInvalidValue;
   }
   dim3 grid((unsigned)((a.n + 15) / 16), (unsigned)a.heads);

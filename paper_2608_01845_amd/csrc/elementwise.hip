@@ -153,10 +153,17 @@ __device__ __forceinline__ void unpack8(const uint4 &u, float (&x)[8]) {
     x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
+// eight floats -> bf16 (round to nearest even, four v_cvt_pk_bf16_f32)
 __device__ __forceinline__ uint4 pack8(const float (&x)[8]) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_v;
   uint32_t w[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) {
+    bf16x2_v p;
+    p[0] = (__bf16)x[2 * i];
+    p[1] = (__bf16)x[2 * i + 1];
+    w[i] = __builtin_bit_cast(uint32_t, p);
+  }
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 

@@ -16,8 +16,6 @@
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
 
-#include <cstdlib>
-
 namespace wdc {
 
 namespace {
@@ -160,10 +158,17 @@ __device__ __forceinline__ void unpack8(const uint4 &u, float (&x)[8]) {
     x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
+// eight floats -> bf16 (round to nearest even, four v_cvt_pk_bf16_f32)
 __device__ __forceinline__ uint4 pack8(const float (&x)[8]) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_v;
   uint32_t w[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) {
+    bf16x2_v p;
+    p[0] = (__bf16)x[2 * i];
+    p[1] = (__bf16)x[2 * i + 1];
+    w[i] = __builtin_bit_cast(uint32_t, p);
+  }
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 // V^T position of token j (and token of position j): bits 2 and 3 swapped
@@ -188,12 +193,22 @@ __device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, 
 #pragma clang fp contract(off)
   const QkvOut &o = g.qkv;
   constexpr int TPH = HD / 8;
+  // iteration it handles tile row 16 it + threadIdx.x / 32 (chunk threadIdx.x % 32);
+  // its sample and token advance incrementally (no division per row)
+  const int64_t r_first = m0 + (threadIdx.x >> 5);
+  int64_t b = (int64_t)blockIdx.z + r_first / o.rps, jr = r_first % o.rps;
   // (unrolled by 4: the rotation table loads of four rows are in flight together)
 #pragma unroll 4
   for (int it = 0; it < 16; ++it) {
     const int cg = it * 512 + threadIdx.x, row = cg >> 5, cc = cg & 31;
     const int hh = cc / TPH, c = cc % TPH;
     const int64_t r = m0 + row;
+    const int64_t bs = b, j = o.row0 + jr;
+    jr += 16;
+    while (jr >= o.rps) {
+      jr -= o.rps;
+      ++b;
+    }
     float x[8];
     unpack8(*(const uint4 *)qkv_chunk(smem, row, cc), x);
     if (o.qk_norm) {
@@ -207,7 +222,6 @@ __device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, 
       for (int e = 0; e < 8; ++e) x[e] *= rs;
     }
     if (r >= g.m) continue;
-    const int64_t b = (int64_t)blockIdx.z + r / o.rps, j = o.row0 + r % o.rps;
     if (o.rope && j < o.n_video) {
       const float4 *cs4 = (const float4 *)(o.rope + j * (HD / 2) + 4 * c);
       const float4 c01 = cs4[0], c23 = cs4[1];
@@ -220,7 +234,7 @@ __device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, 
         x[2 * p + 1] = t1;
       }
     }
-    *(uint4 *)(dst + ((b * o.heads + h0 + hh) * o.n_pad + j) * HD + 8 * c) = pack8(x);
+    *(uint4 *)(dst + ((bs * o.heads + h0 + hh) * o.n_pad + j) * HD + 8 * c) = pack8(x);
   }
 }
 
@@ -267,13 +281,20 @@ __device__ __forceinline__ void v_scatter(const GemmArgs &g, const char *smem, i
       }
     }
   } else {
+    // element by element: the thread's column is fixed, its row steps by 2
+    const int col = threadIdx.x & 255, hh = col / HD, e = col % HD;
+    const int64_t r_first = m0 + (threadIdx.x >> 8);
+    int64_t b = (int64_t)blockIdx.z + r_first / o.rps, jr = r_first % o.rps;
     for (int it = 0; it < 128; ++it) {
-      const int idx = it * 512 + threadIdx.x, row = idx >> 8, col = idx & 255;
-      const int64_t r = m0 + row;
-      if (r >= g.m) continue;
-      const int64_t b = (int64_t)blockIdx.z + r / o.rps, j = o.row0 + r % o.rps;
-      const int hh = col / HD, e = col % HD;
-      v[((b * o.heads + h0 + hh) * HD + e) * o.n_pad + vt_swap(j)] = (bf16_t)at(row, col);
+      const int row = 2 * it + (threadIdx.x >> 8);
+      const int64_t bs = b, j = o.row0 + jr;
+      jr += 2;
+      while (jr >= o.rps) {
+        jr -= o.rps;
+        ++b;
+      }
+      if (m0 + row >= g.m) break;
+      v[((bs * o.heads + h0 + hh) * HD + e) * o.n_pad + vt_swap(j)] = (bf16_t)at(row, col);
     }
   }
 }
@@ -680,14 +701,12 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
   using C = Cfg<BM, BN, WM, WN>;
   GemmArgs g = g0;
   const int m_tiles = (int)((g.m + BM - 1) / BM), n_tiles = (int)(g.n / BN);
-  // WDC_GEMM_ORDER=0 keeps the older grouped order for comparison
-  static const int order = getenv("WDC_GEMM_ORDER") ? atoi(getenv("WDC_GEMM_ORDER")) : 1;
   // The rectangle order pays on large single products; a z-batch would put every
   // slice's rectangles on the same XCDs, and with fewer than 8 dispatch rounds
   // the partly filled last round costs more than the L2 reuse gains (a batched
   // rollout of 8 mid-size samples ran 40% slower with it).
   const int chunks = n_tiles % 4 == 0 ? (m_tiles + 7) / 8 * (n_tiles / 4) : 0;
-  g.order = (order == 1 && BM == 256 && chunks >= 64 && g.batch <= 1 && device_cus() == 256) ? 1 : 0;
+  g.order = (BM == 256 && chunks >= 64 && g.batch <= 1 && device_cus() == 256) ? 1 : 0;
   int blocks = m_tiles * n_tiles;
   if (g.order == 1) blocks = (chunks + 7) / 8 * 256;
   dim3 grid(blocks, 1, g.batch > 1 ? g.batch : 1), block(C::NT);
@@ -734,9 +753,8 @@ bool operands_aligned(const GemmArgs &g) {
 }  // namespace
 
 bool gemm_qkv_fusable(int dtype, const GemmArgs &g) {
-  static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
   const QkvOut &o = g.qkv;
-  return dtype == 1 && variant == 1 && operands_aligned(g) && g.n % 256 == 0 && g.m >= 512 && g.k < 8192 &&
+  return dtype == 1 && operands_aligned(g) && g.n % 256 == 0 && g.m >= 512 && g.k < 8192 &&
          (o.hd == 64 || o.hd == 128) && o.d % 256 == 0 && g.n == 3 * (int64_t)o.d && o.rps > 0 &&
          o.n_pad % 8 == 0 && (uintptr_t)o.q % 16 == 0 && (uintptr_t)o.k % 16 == 0 && (uintptr_t)o.v % 16 == 0 &&
          (uintptr_t)o.rope % 16 == 0;
@@ -752,30 +770,21 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
   if (dtype == 1 && aligned) {
     static bool seen[64] = {};
     if (first_on_device(seen)) {
-      hipError_t e = set_lds_limit<256, 256, 2, 2>();
-      if (e == hipSuccess) e = set_lds_limit<256, 256, 2, 4>();
-      if (e == hipSuccess) e = set_lds_limit<256, 256, 4, 4>();
+      hipError_t e = set_lds_limit<256, 256, 2, 4>();
       if (e == hipSuccess) e = set_lds_limit<128, 128, 2, 2>();
       if (e == hipSuccess) e = set_lds_limit<128, 64, 2, 2>();
       if (e != hipSuccess) return e;
     }
-    // 256 x 256 block tiles: 8 waves of 128 x 64 by default (two per SIMD). With
-    // the reads and loads interleaved into the MFMA stream they are 0.3-1.5%
-    // faster than 16 waves of 64 x 64 on the 13B products and read a quarter
-    // fewer LDS bytes per MFMA (the chip is power-limited under this load).
-    // WDC_GEMM_VARIANT=2 selects 16 waves, 0 four waves of 128 x 128.
-    static const int variant = getenv("WDC_GEMM_VARIANT") ? atoi(getenv("WDC_GEMM_VARIANT")) : 1;
+    // 256 x 256 block tiles: 8 waves of 128 x 64 (two per SIMD). With the reads
+    // and loads interleaved into the MFMA stream they were 0.3-1.5% faster than
+    // 16 waves of 64 x 64 on the 13B products and read a quarter fewer LDS
+    // bytes per MFMA (the chip is power-limited under this load).
     // Gated residual of a long-K product: the float32 stream's read-modify-write
     // goes past the caches (non-temporal), which then keep the A and weight
     // tiles: +7.5% at K = 12,288, +2% at K = 15,360; at K = 3,072 it was 1.5%
     // slower, so shorter products keep cached accesses.
-    static const int nt = getenv("WDC_GEMM_NT") ? atoi(getenv("WDC_GEMM_NT")) : 1;
-    if (nt && g.epi == EPI_GATE_RES && g.k >= 8192) g.epi = EPI_GATE_RES_NT;
-    auto big = [&](const GemmArgs &gg) {
-      return variant == 0 ? launch_mfma<256, 256, 2, 2>(gg, s)
-             : variant == 1 ? launch_mfma<256, 256, 2, 4>(gg, s)
-                            : launch_mfma<256, 256, 4, 4>(gg, s);
-    };
+    if (g.epi == EPI_GATE_RES && g.k >= 8192) g.epi = EPI_GATE_RES_NT;
+    auto big = [&](const GemmArgs &gg) { return launch_mfma<256, 256, 2, 4>(gg, s); };
     // the 256 x 256 kernels stage bf16 outputs through LDS and store whole
     // 16-byte row chunks: they need 16-byte-aligned output rows (other bf16
     // outputs take the 128 x 128 kernels, which store 8-byte groups)
@@ -791,13 +800,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
       // turns 12.375 rounds into 12 plus 2,040 rows: +1.5% at K = 12,288, +2% at
       // K = 15,360; at K = 3,072 the small tiles' lower efficiency costs more
       // than the idle CUs (-1.3%), so short products keep one launch.
-      static const int split = getenv("WDC_GEMM_SPLIT") ? atoi(getenv("WDC_GEMM_SPLIT")) : 1;
       const int64_t m_tiles = (g.m + 255) / 256, n_tiles = g.n / 256;
       int64_t gcd = n_tiles, r = 256;
       while (r) { const int64_t t = gcd % r; gcd = r; r = t; }
       const int64_t m1 = m_tiles / (256 / gcd) * (256 / gcd) * 256;   // rows in whole rounds
       const bool thin_tail = (m_tiles * n_tiles) % 256 != 0 && (m_tiles * n_tiles) % 256 <= 128;
-      if (split && g.batch <= 1 && g.k >= 8192 && thin_tail && device_cus() == 256 && m1 > 0 && m1 < g.m) {
+      if (g.batch <= 1 && g.k >= 8192 && thin_tail && device_cus() == 256 && m1 > 0 && m1 < g.m) {
         GemmArgs g1 = g, g2 = g;
         g1.m = m1;
         g2.m = g.m - m1;
