@@ -396,6 +396,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
         WDC_PPR3_READ(q_ + 4, vb_, kb_)                                                          \
       else  /* the next step's first reads: V^T of tile t + 1, published by the last barrier */  \
         WDC_PPR3_READ(q_ + 4 - NMF, vn_, kb_)                                                    \
+      /* hd 64: the read goes out before the pair (0.8% faster than after it) */                 \
+      if constexpr (EPM == 2) __builtin_amdgcn_sched_barrier(0);                                  \
       if constexpr (EPM == 2) {                                                                  \
         /* both exponentials of a pair, converted together; the empty asm pins */                \
         /* the pair under this MFMA (left free, the compiler sinks all of them */                \
