@@ -124,6 +124,7 @@ struct GemmArgs {
   // block-to-tile order of the MFMA kernels, chosen by launch_gemm: 0 groups
   // of 8 M tiles, 1 one 8 x 4 tile rectangle per XCD per dispatch round
   int order;
+  int rect_n;        // order 1: N tiles of the rectangle (32 / rect_n M tiles)
   QkvOut qkv;        // EPI_QKV only
 };
 

@@ -328,13 +328,15 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
   int mt, nt;
   if (g.order == 1) {
     // Dispatch rounds of 256 blocks, one per CU; block id % 8 is its XCD. Round
-    // r gives XCD x chunk 8r + x: an 8 (M) x 4 (N) rectangle of tiles, one per
-    // block, so the 32 blocks an XCD runs together start together and share 8 A
-    // slices and 4 weight slices in its L2. Blocks past the last tile exit.
+    // r gives XCD x chunk 8r + x: a (32 / rect_n) (M) x rect_n (N) rectangle of
+    // tiles (8 x 4 or 2 x 16), one per block, so the 32 blocks an XCD runs
+    // together start together and share their A and weight slices in its L2.
+    // Blocks past the last tile exit.
     const int r = bid / 256, x = bid % 8, l = (bid / 8) % 32;
-    const int chunk = 8 * r + x, cpb = n_tiles / 4;
-    mt = 8 * (chunk / cpb) + l % 8;
-    nt = 4 * (chunk % cpb) + l / 8;
+    const int rn = g.rect_n, rm = 32 / rn;
+    const int chunk = 8 * r + x, cpb = n_tiles / rn;
+    mt = rm * (chunk / cpb) + l % rm;
+    nt = rn * (chunk % cpb) + l / rm;
     if (mt >= m_tiles) return;
   } else if (gsize == group && n_tiles >= 24) {
     // Workgroups go to the 8 XCDs round robin (id % 8). Give each XCD a
@@ -705,7 +707,12 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
   // slice's rectangles on the same XCDs, and with fewer than 8 dispatch rounds
   // the partly filled last round costs more than the L2 reuse gains (a batched
   // rollout of 8 mid-size samples ran 40% slower with it).
-  const int chunks = n_tiles % 4 == 0 ? (m_tiles + 7) / 8 * (n_tiles / 4) : 0;
+  // 2 x 16 rectangles where the N tiles allow it: A panels (the activations,
+  // larger than the last-level cache) are re-read from HBM once per rectangle
+  // column, weight panels (which fit that cache) once per rectangle row; at
+  // N = 12,288 that was 2.5-3% faster than 8 x 4 on the product alone
+  g.rect_n = n_tiles % 16 == 0 ? 16 : 4;
+  const int chunks = n_tiles % g.rect_n == 0 ? (m_tiles + 32 / g.rect_n - 1) / (32 / g.rect_n) * (n_tiles / g.rect_n) : 0;
   g.order = (BM == 256 && chunks >= 64 && g.batch <= 1 && device_cus() == 256) ? 1 : 0;
   int blocks = m_tiles * n_tiles;
   if (g.order == 1) blocks = (chunks + 7) / 8 * 256;
