@@ -707,11 +707,11 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
   // slice's rectangles on the same XCDs, and with fewer than 8 dispatch rounds
   // the partly filled last round costs more than the L2 reuse gains (a batched
   // rollout of 8 mid-size samples ran 40% slower with it).
-  // 2 x 16 rectangles where the N tiles allow it: A panels (the activations,
-  // larger than the last-level cache) are re-read from HBM once per rectangle
-  // column, weight panels (which fit that cache) once per rectangle row; at
-  // N = 12,288 that was 2.5-3% faster than 8 x 4 on the product alone
-  g.rect_n = n_tiles % 16 == 0 ? 16 : 4;
+  // 8 x 4 rectangles. 2 x 16 ones (A panels, larger than the last-level cache,
+  // re-read once per rectangle column; weight panels, which fit it, once per
+  // rectangle row) made the N = 12,288 product 2.5-3% faster alone but the
+  // whole 13B forward's GEMMs 1% slower (same-box A/B), so they are not used.
+  g.rect_n = 4;
   const int chunks = n_tiles % g.rect_n == 0 ? (m_tiles + 32 / g.rect_n - 1) / (32 / g.rect_n) * (n_tiles / g.rect_n) : 0;
   g.order = (BM == 256 && chunks >= 64 && g.batch <= 1 && device_cus() == 256) ? 1 : 0;
   int blocks = m_tiles * n_tiles;

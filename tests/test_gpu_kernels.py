@@ -80,11 +80,11 @@ def test_linear_output_rows_not_16_byte_aligned():
 
 @pytest.mark.parametrize("n", [8192, 9216])
 def test_linear_large_product_rectangle_order(n):
-    """Products big enough for the XCD-rectangle block order, with blocks past
-    the last tile in the final dispatch round: 32 N tiles take 2 x 16
-    rectangles (65 M tiles in 33 bands, the last one partial), 36 N tiles
-    take 8 x 4 ones (9 bands, the last one partial). Sampled rows, including
-    every row of the partial band, against the oracle."""
+    """Products big enough for the XCD-rectangle block order (8 x 4 tiles per
+    XCD per dispatch round: 65 M tiles in 9 bands, the last one partial, x 32
+    or 36 N tiles), with blocks past the last tile in the final dispatch round.
+    Sampled rows, including every row of the partial band, against the oracle;
+    the whole output against a float32 product."""
     torch = torch_cuda()
     cfg = synth.get_config("mid")
     ctx = context(cfg, weights=False)
