@@ -65,6 +65,10 @@ def parse():
     ap.add_argument("--stress-only", action="store_true",
                     help="run only the 118,800-token legs (attention alone, one single-stream block) and print "
                          "their JSON")
+    ap.add_argument("--no-library", action="store_true",
+                    help="skip the same-box comparison with torch's attention and F.linear")
+    ap.add_argument("--library-only", action="store_true",
+                    help="run only that comparison (on the workload's shapes) and print its JSON")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="also run one plain device copy of this many bytes (hardware-counter calibration)")
     return ap.parse_args()
@@ -295,6 +299,84 @@ def stress_leg(wdc, synth, torch, dev, reps=3):
             "attention_alone": att, "single_block": blk}
 
 
+def library_leg(wdc, cfg, torch, dev, reps=3):
+    """Same-box context for the two dominant kernels: this library's attention
+    and plain bf16 product (bias add, no fused epilogue) against torch's
+    scaled_dot_product_attention (flash backend) and F.linear on the same
+    shapes and inputs, all timed with events on the current stream (the
+    library's stream). The library numbers are the product path; torch's are
+    context, not a target."""
+    import torch.nn.functional as F
+    ctx = wdc.Context(cfg, device=str(dev), allocate_weights=False)
+    gen = torch.Generator(device=dev).manual_seed(cfg.seed + 7)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    def entry(flop, ms_lib, ms_torch, err):
+        return {"ms": round(ms_lib, 3), "tflops": round(flop / ms_lib / 1e9, 1),
+                "torch_ms": round(ms_torch, 3) if ms_torch else None,
+                "torch_tflops": round(flop / ms_torch / 1e9, 1) if ms_torch else None,
+                "speedup_vs_torch": round(ms_torch / ms_lib, 3) if ms_torch else None,
+                "rel_l2_vs_torch": float(f"{err:.2e}") if err is not None else None}
+
+    out = {}
+    n, h, hd = cfg.n_tokens, cfg.heads, cfg.head_dim
+    npad = ctx.attn_pad(n)
+    q = torch.zeros((h, npad, hd), dtype=torch.bfloat16, device=dev)
+    k, v = torch.zeros_like(q), torch.zeros_like(q)
+    for x in (q, k, v):
+        x[:, :n] = torch.randn((h, n, hd), generator=gen, device=dev).to(torch.bfloat16)
+    # V^T with the key order the kernel takes: within each group of 16 keys,
+    # key j sits at column j with bits 2 and 3 swapped
+    j = torch.arange(npad, device=dev)
+    col = (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1)
+    vt = torch.empty((h, hd, npad), dtype=torch.bfloat16, device=dev)
+    vt[:, :, col] = v.transpose(1, 2)
+    o = torch.empty((n, h * hd), dtype=torch.bfloat16, device=dev)
+    ms_lib = timed(lambda: ctx.attention(q, k, vt, n, o, h * hd))
+    q4, k4, v4 = (x[:, :n].unsqueeze(0) for x in (q, k, v))
+    ms_t, err, note = None, None, None
+    try:
+        with torch.nn.attention.sdpa_kernel(torch.nn.attention.SDPBackend.FLASH_ATTENTION):
+            ms_t = timed(lambda: F.scaled_dot_product_attention(q4, k4, v4))
+            ref = F.scaled_dot_product_attention(q4, k4, v4)[0].transpose(0, 1).reshape(n, h * hd).float()
+        err = ((o.float() - ref).norm() / ref.norm()).item()
+        del ref
+    except Exception as e:  # a torch build without the flash backend: report the library alone
+        note = f"torch flash attention unavailable: {str(e)[:100]}"
+    out["attention"] = entry(4.0 * n * n * hd * h, ms_lib, ms_t, err)
+    if note:
+        out["attention"]["note"] = note
+    del q, k, v, vt, o, q4, k4, v4
+    torch.cuda.empty_cache()
+    d, f = cfg.hidden, cfg.mlp_ratio * cfg.hidden
+    for name, (nn_, kk) in (("qkv", (3 * d, d)), ("mlp_in", (f, d)), ("single_out", (d, d + f)),
+                            ("mlp_out", (d, f)), ("attn_out", (d, d))):
+        a = torch.randn((n, kk), generator=gen, device=dev).to(torch.bfloat16)
+        w = (0.02 * torch.randn((nn_, kk), generator=gen, device=dev)).to(torch.bfloat16)
+        b = (0.1 * torch.randn((nn_,), generator=gen, device=dev)).to(torch.bfloat16)
+        c = torch.empty((n, nn_), dtype=torch.bfloat16, device=dev)
+        ms_lib = timed(lambda: ctx.linear(a, w, b, c, n, nn_, kk))
+        ms_t = timed(lambda: F.linear(a, w, b))
+        ref = F.linear(a, w, b).float()
+        err = ((c.float() - ref).norm() / ref.norm()).item()
+        out[f"linear_{name}"] = dict(entry(2.0 * n * nn_ * kk, ms_lib, ms_t, err), shape=[n, nn_, kk])
+        del a, w, b, c, ref
+        torch.cuda.empty_cache()
+    del ctx
+    torch.cuda.empty_cache()
+    return out
+
+
 def batched_leg(wdc, synth, torch, dev, steps=20, batches=(1, 8)):
     """Throughput of batched rollouts on the mid workload (8 blocks, D = 1024, 2,688
     tokens, bf16): B independent all-exact rollouts of `steps` denoising steps, F_theta
@@ -349,6 +431,9 @@ def main():
         return
     if args.stress_only:
         print(json.dumps({"stress_118800": stress_leg(wdc, synth, torch, dev)}), flush=True)
+        return
+    if args.library_only:
+        print(json.dumps({"library_comparison": library_leg(wdc, cfg, torch, dev)}), flush=True)
         return
     S = cfg.steps
     log(f"workload {cfg.name}: {cfg.n_blocks} blocks, N={cfg.n_tokens}, D={cfg.hidden}, {cfg.heads}x{cfg.head_dim}")
@@ -477,6 +562,9 @@ def main():
         out["stress_118800"] = stress_leg(wdc, synth, torch, dev)
     if not args.no_surrogate:
         out["surrogate_kernels"] = surrogate_leg(wdc, synth, torch, dev)
+    if not args.no_library:
+        log("same-box comparison with torch's attention and products ...")
+        out["library_comparison"] = library_leg(wdc, cfg, torch, dev)
     if not args.no_batch:
         log("batched rollouts (mid workload) ...")
         out["batched_rollout"] = batched_leg(wdc, synth, torch, dev)
