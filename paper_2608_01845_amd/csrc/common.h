@@ -125,6 +125,10 @@ struct GemmArgs {
   // of 8 M tiles, 1 one 8 x 4 tile rectangle per XCD per dispatch round
   int order;
   int rect_n;        // order 1: N tiles of the rectangle (32 / rect_n M tiles)
+  // 1: a product whose 256 x 256 tiles would fill less than one dispatch round
+  // (fewer tiles than compute units) runs on 128 x 128 tiles, four times the
+  // blocks; 0: the tile size follows the shape alone
+  int fill_tiles;
   QkvOut qkv;        // EPI_QKV only
 };
 

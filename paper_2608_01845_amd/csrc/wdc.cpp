@@ -60,6 +60,10 @@ struct wdc_ctx {
   // q/k/v preparation in the projection's epilogue where the GEMM allows it
   // (WDC_FUSE_QKV=0: always the separate kernels, for comparison)
   bool fuse_qkv = true;
+  // products that would not fill one dispatch round of 256 x 256 tiles run on
+  // 128 x 128 tiles (WDC_FILL_TILES=0: tile size by shape alone, so tests can
+  // reach the 256 x 256 kernels and the fused q/k/v epilogue at small sizes)
+  bool fill_tiles = true;
   // timing
   bool timing = false;
   std::vector<TimedEvent> events;
@@ -300,6 +304,7 @@ wdc_status gemm(wdc_ctx *c, const void *a, int64_t lda, const void *w, const voi
   g.a_bs = bt.a_bs;
   g.c_bs = bt.c_bs;
   g.gate_bs = bt.gate_bs;
+  g.fill_tiles = c->fill_tiles;
   HIPCHK(c, timed(c, WDC_T_GEMM, 2.0 * m * n * k * bt.n, [&] { return launch_gemm(c->d.dtype, g, c->stream); }));
   return WDC_OK;
 }
@@ -391,6 +396,7 @@ wdc_status qkv_project(wdc_ctx *c, const void *a, const void *w, const void *bia
   g.n = 3 * D;
   g.k = D;
   g.epi = EPI_QKV;
+  g.fill_tiles = c->fill_tiles;
   g.batch = batched ? (int)NB : 1;
   g.a_bs = batched ? N * D : 0;
   QkvOut &o = g.qkv;
@@ -1111,6 +1117,7 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
   }
   c->mb = d.max_batch > 1 ? d.max_batch : 1;
   c->fuse_qkv = !(getenv("WDC_FUSE_QKV") && atoi(getenv("WDC_FUSE_QKV")) == 0);
+  c->fill_tiles = !(getenv("WDC_FILL_TILES") && atoi(getenv("WDC_FILL_TILES")) == 0);
   c->stream = (hipStream_t)stream;
   c->esz = d.dtype == WDC_BF16 ? 2 : 4;
   c->D = d.hidden;

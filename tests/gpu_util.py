@@ -1,6 +1,8 @@
 """Shared helpers of the GPU parity tests (seeded inputs, tolerances, contexts)."""
 from __future__ import annotations
 
+import os
+
 import numpy as np
 import pytest
 
@@ -62,10 +64,18 @@ def wdc_params(p):
     return out
 
 
-def context(cfg, weights=True, params=None):
+def context(cfg, weights=True, params=None, fill_tiles=True):
+    """A context on cuda:0. fill_tiles=False: GEMM tile size by shape alone
+    (products too small to fill one dispatch round of 256 x 256 tiles keep
+    those tiles instead of moving to 128 x 128 ones)."""
     torch = torch_cuda()
     import paper_2608_01845_amd as wdc
-    ctx = wdc.Context(cfg, params=params, allocate_weights=weights)
+    if not fill_tiles:
+        os.environ["WDC_FILL_TILES"] = "0"
+    try:
+        ctx = wdc.Context(cfg, params=params, allocate_weights=weights)
+    finally:
+        os.environ.pop("WDC_FILL_TILES", None)
     if weights:
         ctx.load_weights(synth.gen_weights(cfg))
     return ctx

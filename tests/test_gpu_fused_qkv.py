@@ -17,9 +17,16 @@ pytestmark = pytest.mark.gpu
 
 
 def _pair(cfg, max_batch=1):
-    """(fused, separate) contexts sharing one weight blob."""
+    """(fused, separate) contexts sharing one weight blob. These products are
+    too small to fill a dispatch round of 256 x 256 tiles, which would send
+    them to the 128 x 128 tiles and the separate kernels: the fused context
+    keeps the tile size the shape selects (WDC_FILL_TILES=0)."""
     import paper_2608_01845_amd as wdc
-    fused = wdc.Context(cfg, max_batch=max_batch)
+    os.environ["WDC_FILL_TILES"] = "0"
+    try:
+        fused = wdc.Context(cfg, max_batch=max_batch)
+    finally:
+        del os.environ["WDC_FILL_TILES"]
     fused.load_weights(synth.gen_weights(cfg))
     os.environ["WDC_FUSE_QKV"] = "0"
     try:
@@ -72,3 +79,29 @@ def test_fused_qkv_batched_forward_equals_separate_preparation():
     for a, b in zip(vf, vs):
         print("batched forward: fused vs separate max |diff|", float((a - b).abs().max()))
         assert torch.isfinite(a).all() and torch.equal(a, b)
+
+
+def test_fill_tiles_mid_forward_bitwise_equal():
+    """The mid-size forward (2,688 tokens, D = 1,024) with its products on 128 x
+    128 tiles and the separate q/k/v preparation (the default: no product fills
+    a dispatch round of 256 x 256 tiles) against the 256 x 256 tiles and the
+    fused epilogue: both sum every output over K in the same order and apply
+    the same float32 arithmetic afterwards, so the velocities agree bit for bit."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config("mid")
+    fill = wdc.Context(cfg)
+    fill.init_random_weights(seed=5, std=0.02)
+    os.environ["WDC_FILL_TILES"] = "0"
+    try:
+        shape = wdc.Context(cfg, allocate_weights=False)
+    finally:
+        del os.environ["WDC_FILL_TILES"]
+    shape.bind_weights(fill.weights)
+    inp = synth.gen_inputs(cfg)
+    z = torch.from_numpy(inp["z_T"]).cuda()
+    cond = fill.to_device(inp["cond"])
+    a = fill.forward(z, 0.7, cond)
+    b = shape.forward(z, 0.7, cond)
+    print("mid forward: 128 x 128 + separate vs 256 x 256 + fused max |diff|", float((a - b).abs().max()))
+    assert torch.isfinite(a).all() and torch.equal(a, b)

@@ -33,15 +33,20 @@ def test_scheduler_step_matches_closed_form():
         assert np.max(np.abs(out - ref)) <= 1e-6 * (1 + np.abs(ref).max())
 
 
+@pytest.mark.parametrize("fill_tiles", [True, False])
 @pytest.mark.parametrize("dtype,m,n,k", [
     ("bf16", 1000, 512, 3072), ("bf16", 600, 768, 1024), ("bf16", 300, 256, 128), ("bf16", 130, 384, 64),
     ("bf16", 37, 64, 64), ("bf16", 700, 64, 1024), ("bf16", 67, 192, 512), ("bf16", 1, 128, 256),
     ("bf16", 700, 2048, 256), ("bf16", 2100, 4096, 128),
     ("f32", 300, 320, 96), ("f32", 5, 64, 256)])
-def test_linear_matches_oracle(dtype, m, n, k):
+def test_linear_matches_oracle(dtype, m, n, k, fill_tiles):
+    """fill_tiles=True: these products fill less than one dispatch round of
+    256 x 256 tiles, so those with N % 128 == 0 run on 128 x 128 tiles; False:
+    the same products on the tiles their shape alone selects (256 x 256 where
+    N % 256 == 0 and M >= 512), so both kernels meet ragged M tails."""
     torch = torch_cuda()
     cfg = synth.get_config("mid" if dtype == "bf16" else "tiny")
-    ctx = context(cfg, weights=False)
+    ctx = context(cfg, weights=False, fill_tiles=fill_tiles)
     rng = _rng(m * 7 + n)
     a = synth.stored(rng.standard_normal((m, k)), cfg.dtype)
     w = synth.stored(rng.standard_normal((n, k)) * 0.05, cfg.dtype)
@@ -59,12 +64,12 @@ def test_linear_matches_oracle(dtype, m, n, k):
 
 def test_linear_output_rows_not_16_byte_aligned():
     """bf16 output rows 8-byte but not 16-byte aligned (ldc = n + 4): the
-    product would take the 256 x 256 kernels, whose staged epilogue stores
-    16-byte chunks, so it must run on the 128 x 128 kernels instead. Columns
-    past n stay untouched."""
+    product would take the 256 x 256 kernels (tile size by shape alone), whose
+    staged epilogue stores 16-byte chunks, so it must run on the 128 x 128
+    kernels instead. Columns past n stay untouched."""
     torch = torch_cuda()
     cfg = synth.get_config("mid")
-    ctx = context(cfg, weights=False)
+    ctx = context(cfg, weights=False, fill_tiles=False)
     m, n, k = 600, 512, 256
     rng = _rng(77)
     a = synth.stored(rng.standard_normal((m, k)), cfg.dtype)
