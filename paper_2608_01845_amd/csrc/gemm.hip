@@ -11,7 +11,9 @@
 // one read at a time between its MFMAs, and the stage barrier sits before a
 // stage's last k-step so the matrix cores never drain at it. Large single
 // products take an XCD-aware block order, and long-K ones whose last dispatch
-// round would be thin run their last rows as a second launch of 128 x 128 tiles.
+// round would be thin run their last rows as a second launch of 128 x 128 tiles;
+// products too small to fill one dispatch round of 256 x 256 tiles run on
+// 128 x 128 tiles throughout.
 // float32 path (tiny fp32 workload, and shapes the MFMA tiles do not cover):
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
