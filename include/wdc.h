@@ -142,7 +142,10 @@ typedef struct {
 void wdc_params_default(wdc_params *p);
 
 /* Create a context for one model on one stream (the current HIP device).
- * desc may describe zero blocks (surrogate-only use). */
+ * desc may describe zero blocks (surrogate-only use). bf16: WDC_E_SHAPE if
+ * the joint sequence (video + text tokens, padded) holds more than 2^30 bytes
+ * per head of q, k or v (about 4.2 million tokens at head size 128): the bf16
+ * attention kernel addresses one head's rows with 32-bit offsets. */
 wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_stream stream, wdc_ctx **out);
 wdc_status wdc_destroy(wdc_ctx *ctx);
 /* Message of the last failure on this context ("" if none). ctx may be NULL
@@ -290,7 +293,8 @@ wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, 
  * (keys) >= n of q/k/v must be zero. d_o: [n, ldo], head h written at columns
  * [h*hd, (h+1)*hd); ldo >= heads*hd (else WDC_E_ARG). q, k, vt 16-byte
  * aligned; for bf16 d_o 8-byte aligned and ldo a multiple of 4 (else
- * WDC_E_ALIGN). */
+ * WDC_E_ALIGN); bf16 with n_pad * hd * 2 above 2^30 bytes (32-bit offsets
+ * within a head) is WDC_E_SHAPE. */
 int64_t wdc_attn_pad(int64_t n);
 wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
                          int64_t ldo);

@@ -162,6 +162,9 @@ struct AttnArgs {
   int hpb;
 };
 int64_t attn_pad(int64_t n);
+// The bf16 attention kernel addresses one head's padded rows of q, k and v^T
+// with 32-bit byte offsets (buffer ranges, tile offsets): keep a head within 2^30 B.
+inline bool attn_len_ok(int64_t n, int hd) { return attn_pad(n) * hd * 2 <= (int64_t(1) << 30); }
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
 
 // ------------------------------------------------------------------ elementwise and small kernels

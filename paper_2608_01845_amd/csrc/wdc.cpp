@@ -1129,6 +1129,11 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
   c->nt = d.text_tokens;
   c->n = c->nv + c->nt;
   c->n_pad = attn_pad(c->n);
+  if (nblocks > 0 && d.dtype == WDC_BF16 && !attn_len_ok(c->n, c->hd)) {
+    g_create_err = "sequence too long: one head's q, k or v would exceed 2^30 bytes (32-bit offsets)";
+    delete c;
+    return WDC_E_SHAPE;
+  }
   c->T = (int64_t)d.lat_f * d.lat_h * d.lat_w;
   c->E = (int64_t)d.lat_c * c->T;
   if (nblocks > 0) build_layout(c);
@@ -1549,6 +1554,7 @@ wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const v
                          int64_t ldo) {
   if (!ctx || !d_q || !d_k || !d_vt || !d_o || n <= 0) return WDC_E_ARG;
   if (ldo < (int64_t)ctx->H * ctx->hd) return WDC_E_ARG;     // heads would overlap and the last row overrun
+  if (ctx->d.dtype == WDC_BF16 && !attn_len_ok(n, ctx->hd)) return WDC_E_SHAPE;
   if (!aligned16(d_q) || !aligned16(d_k) || !aligned16(d_vt)) return WDC_E_ALIGN;
   // bf16 rows leave as 8-byte groups of 4 columns
   if (ctx->d.dtype == WDC_BF16 && ((uintptr_t)d_o % 8 != 0 || ldo % 4 != 0)) return WDC_E_ALIGN;

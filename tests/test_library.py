@@ -124,6 +124,8 @@ def test_create_rejects_bad_descriptors(wdc):
         synth.get_config("tiny", latent=(16, 4, 15, 16)),           # not divisible by the patch
         synth.get_config("tiny", rope=(16, 24, 22)),                # rotary dims do not sum to head_dim
         synth.get_config("tiny", n_dual=1),                         # dual-stream blocks without text
+        # bf16, 4,200,000 tokens at head size 128: one head's q would pass 2^30 bytes
+        synth.get_config("tiny", dtype="bf16", heads=2, head_dim=128, rope=(16, 56, 56), latent=(16, 100, 300, 560)),
     ]
     for cfg in bad:
         d = wdc.desc_from_config(cfg)
@@ -132,6 +134,14 @@ def test_create_rejects_bad_descriptors(wdc):
         st = lib.wdc_create(C.byref(d), C.byref(p), None, C.byref(h))
         assert st != 0
         assert lib.wdc_last_error(None)
+    # under the limit (4,110,000 tokens), and float32 past it, are accepted
+    for cfg in (synth.get_config("tiny", dtype="bf16", heads=2, head_dim=128, rope=(16, 56, 56),
+                                 latent=(16, 100, 300, 548)),
+                synth.get_config("tiny", heads=2, head_dim=128, rope=(16, 56, 56), latent=(16, 100, 300, 560))):
+        d = wdc.desc_from_config(cfg)
+        assert lib.wdc_create(C.byref(d), C.byref(wdc.default_params()), None, C.byref(h)) == 0, \
+            lib.wdc_last_error(None)
+        lib.wdc_destroy(h)
     p = wdc.default_params(bank_capacity=9)
     d = wdc.desc_from_config(synth.get_config("tiny"))
     h = C.c_void_p()
