@@ -21,10 +21,12 @@ Modules
 Where the paper defers details to its supplementary material, the reading
 used is recorded in ``params.DEFAULTS`` and in the module docstrings.
 
-Parity unpinned: ``dit.dit_forward`` as a composed whole (each operation and
-block is pinned, but a random-init model has no value the paper fixes), and
-the numerical values the diagnostics produce on such a model (the paper's
-correlations and false-safe rates come from trained models); the diagnostics'
-own arithmetic is pinned.
+Pins: every operation, block and the composed ``dit.dit_forward`` is pinned
+(library routines, closed forms, brute force, an independent torch
+composition, and invariants the architecture fixes: head relabelling,
+text-token order, zero residual gates). A random-init model has no output
+value the paper prints, and the paper's correlations and false-safe rates come
+from trained models, so the values the diagnostics produce here are not
+compared with the paper's; the diagnostics' arithmetic is pinned.
 """
 from . import params, dit, scheduler, surrogate, risk, rollout  # noqa: F401

@@ -411,3 +411,123 @@ def test_output_head_matches_torch():
     fp, hp, wp = cfg.grid
     ref = einops.rearrange(out, "(f h w) (c a i j) -> c (f a) (h i) (w j)", f=fp, h=hp, w=wp, c=16, a=1, i=2, j=2)
     np.testing.assert_allclose(dit.final_layer(W, cfg, x, c), ref, atol=1e-12 * np.abs(ref).max())
+
+
+# --------------------------------------------------------------------------- whole-forward invariants
+
+def _head_permuted(W, cfg, perm):
+    """The weights with the attention heads relabelled by ``perm``: the q, k and v
+    output rows of every projection move by whole heads, and the attention-output
+    columns of every output projection follow. The model is unchanged."""
+    d, hd = cfg.hidden, cfg.head_dim
+    cols = np.concatenate([np.arange(p * hd, (p + 1) * hd) for p in perm])
+    rows = np.concatenate([cols, d + cols, 2 * d + cols])
+    V = dict(W)
+    for name in W:
+        if name.endswith((".qkv.w", ".qkv.b")):
+            V[name] = W[name][rows]
+        elif name.endswith(".lin1.w") or name.endswith(".lin1.b"):
+            V[name] = np.concatenate([W[name][rows], W[name][3 * d:]])
+        elif name.endswith(".out.w"):
+            V[name] = W[name][:, cols]
+        elif name.endswith(".lin2.w"):
+            V[name] = np.concatenate([W[name][:, cols], W[name][:, d:]], axis=1)
+    return V
+
+
+def test_dit_forward_invariant_to_head_relabelling():
+    """Per-head RMSNorm and RoPE act alike on every head and the joint attention
+    is per head, so relabelling the heads consistently in every block (both
+    streams of the dual block included) leaves F_theta unchanged; a mismatch
+    between the head split and the head merge, or streams split differently,
+    breaks it."""
+    cfg = small_cfg(heads=4, head_dim=16, rope=(4, 6, 6))
+    W = {k: v.astype(np.float64) * 5 for k, v in synth.gen_weights(cfg).items()}
+    inp = synth.gen_inputs(cfg)
+    args = (inp["z_T"], 0.4, inp["cond"], inp["text"], inp["cam"])
+    ref = dit.dit_forward(W, cfg, *args)
+    got = dit.dit_forward(_head_permuted(W, cfg, [2, 0, 3, 1]), cfg, *args)
+    assert np.abs(ref).max() > 1e-2
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-10 * np.abs(ref).max())
+    # a relabelling of the q/k rows alone (v and the output columns left) is a different model
+    bad = dict(W)
+    for name in W:
+        if name.endswith((".qkv.w", ".qkv.b")):
+            d, hd = cfg.hidden, cfg.head_dim
+            cols = np.concatenate([np.arange(p * hd, (p + 1) * hd) for p in [2, 0, 3, 1]])
+            bad[name] = W[name][np.concatenate([cols, d + cols, 2 * d + np.arange(d)])]
+    assert np.abs(dit.dit_forward(bad, cfg, *args) - ref).max() > 1e-3 * np.abs(ref).max()
+
+
+def test_dit_forward_invariant_to_text_token_order():
+    """Text tokens carry no position (RoPE rotates the video rows only) and every
+    video query attends over the joint set of keys, so reordering the text
+    tokens leaves the velocity unchanged; giving text rows a position or
+    attending over the video rows alone would break it (the second is checked:
+    dropping the text changes the velocity)."""
+    cfg = small_cfg(text_tokens=5)
+    W = {k: v.astype(np.float64) * 5 for k, v in synth.gen_weights(cfg).items()}
+    inp = synth.gen_inputs(cfg)
+    text = inp["text"]
+    ref = dit.dit_forward(W, cfg, inp["z_T"], 0.7, inp["cond"], text, inp["cam"])
+    got = dit.dit_forward(W, cfg, inp["z_T"], 0.7, inp["cond"], text[[3, 0, 4, 2, 1]], inp["cam"])
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-10 * np.abs(ref).max())
+    other = dit.dit_forward(W, cfg, inp["z_T"], 0.7, inp["cond"], 2.0 * text, inp["cam"])
+    assert np.abs(other - ref).max() > 1e-3 * np.abs(ref).max()
+
+
+def test_dit_forward_with_zero_gates_is_the_output_head_on_the_embedding():
+    """With every block's residual gates zero (their adaLN rows and biases zeroed,
+    shift and scale left as they are) each block returns its input, so F_theta
+    reduces to the output head applied to the patch embedding; a block that
+    added its branch ungated, or replaced the stream by its modulated input,
+    would not."""
+    cfg = small_cfg()
+    W = {k: v.astype(np.float64) * 5 for k, v in synth.gen_weights(cfg).items()}
+    d = cfg.hidden
+    for name in list(W):
+        if name.endswith((".ada.w", ".ada.b")) and not name.startswith("final"):
+            gates = [2] if name.startswith("single") else [2, 5]
+            W[name] = W[name].copy()
+            for g in gates:
+                W[name][g * d:(g + 1) * d] = 0.0
+    inp = synth.gen_inputs(cfg)
+    args = (inp["z_T"], 0.55, inp["cond"], inp["text"], inp["cam"])
+    got = dit.dit_forward(W, cfg, *args)
+    c_emb = dit.cond_embedding(W, cfg, 0.55, inp["cond"], inp["cam"])
+    tokens = dit.patchify(np.asarray(inp["z_T"], np.float64), cfg.patch) @ W["patch_embed.w"].T + W["patch_embed.b"]
+    ref = dit.final_layer(W, cfg, tokens, c_emb)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12 * np.abs(ref).max())
+
+
+def _merge_interleaved(x):
+    h, n, hd = x.shape
+    return x.transpose(1, 2, 0).reshape(n, h * hd)
+
+
+def _rope_on_text(cfg, n_rows):
+    idx = np.arange(n_rows)
+    return np.where(idx < cfg.n_video, idx, idx % cfg.n_video)
+
+
+_single_block = dit.single_block
+
+
+def _single_stream_replaced(W, cfg, pre, x, c_emb, rows=None):
+    sh, sc, _ = np.split(dit.linear(W, pre + ".ada", dit.silu(c_emb)), 3)
+    return _single_block(W, cfg, pre, x, c_emb, rows) + dit.modulate(dit.layer_norm(x), sh, sc) - x
+
+
+@pytest.mark.parametrize("target,mistake,test", [
+    ("_merge", _merge_interleaved, test_dit_forward_invariant_to_head_relabelling),
+    ("_rope_index", _rope_on_text, test_dit_forward_invariant_to_text_token_order),
+    ("single_block", _single_stream_replaced, test_dit_forward_with_zero_gates_is_the_output_head_on_the_embedding),
+])
+def test_whole_forward_invariants_catch_planted_mistakes(monkeypatch, target, mistake, test):
+    """Each whole-forward invariant fails on the oracle with a plausible mistake
+    planted: heads merged in an interleaved order after a contiguous split,
+    text rows rotated as if they had video positions, a single-stream block
+    whose stream is replaced by its modulated input."""
+    monkeypatch.setattr(dit, target, mistake)
+    with pytest.raises(AssertionError):
+        test()
