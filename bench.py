@@ -477,6 +477,11 @@ def main():
         log(f"timed step {i + 1}/{args.steps} done ({time.perf_counter() - t0:.2f}s)")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    # device memory of the exact steps: the library's weights, workspace and
+    # rollout state all come from torch allocations
+    free_b, total_b = torch.cuda.mem_get_info(dev)
+    memory = {"peak_allocated_gb": round(torch.cuda.max_memory_allocated(dev) / 1e9, 2),
+              "device_used_gb": round((total_b - free_b) / 1e9, 2), "device_total_gb": round(total_b / 1e9, 1)}
     timing = ctx.timing()
     ctx.set_timing(False)
     ms_step = elapsed / args.steps * 1e3
@@ -529,6 +534,7 @@ def main():
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "denoising_steps_per_s_exact": round(1e3 / ms_step, 4),
         "surrogate_step_ms": round(sur_med, 3),
+        "memory": memory,
         "derived_rollout_estimate": {"steps": S, "exact_ratio": exact_ratio, "seconds": round(derived_rollout_s, 2),
                                      "steps_per_s": round(S / derived_rollout_s, 3),
                                      "note": "arithmetic on the measured exact-step and surrogate-step times, "
