@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--stress-only", action="store_true",
                     help="run only the 118,800-token legs (attention alone, one single-stream block) and print "
                          "their JSON")
+    ap.add_argument("--no-5b", action="store_true",
+                    help="skip the 5B-shaped exact steps and risk-controlled rollout")
     ap.add_argument("--no-library", action="store_true",
                     help="skip the same-box comparison with torch's attention and F.linear")
     ap.add_argument("--library-only", action="store_true",
@@ -241,6 +243,63 @@ def rollout_leg(wdc, cfg, ctx, inp, torch, dev, tau=None, period=5):
         res["placement"] = f"periodic, exact when k mod {period} == 0 (surrogate elsewhere when available)"
     del rctx, st, z
     return res
+
+
+def second_workload_leg(wdc, synth, torch, dev, name="5b", steps=3):
+    """The other model class of the paper's generation experiments (the 5B shape:
+    30 sequential blocks over the joint sequence, D = 3,072, 48 x 64 heads,
+    17,550 video + 226 text tokens): exact denoising steps timed as in the main measurement (one
+    warm-up step, then ``steps`` steps: candidate, risk decision, F_theta, Psi,
+    counterfactual and insert), with the attention and GEMM classes timed by
+    the library's HIP events, then one measured risk-controlled rollout at the
+    threshold giving that class's exact-call ratio (Sec. 5.1: 47%)."""
+    cfg = synth.get_config(name)
+    ctx = wdc.Context(cfg, device=str(dev))
+    ctx.init_random_weights(seed=1234, std=0.02)
+    st = ctx.new_state()
+    inp = synth.gen_inputs(cfg)
+    dv = {k: ctx.to_device(inp[k]) if k in inp else None for k in ("cond", "text", "cam")}
+    zb = [torch.from_numpy(inp["z_T"]).to(dev), None]
+    zb[1] = torch.empty_like(zb[0])
+    zhat, v = torch.empty_like(zb[0]), torch.empty_like(zb[0])
+    S = cfg.steps
+
+    def exact_step(k, cur):
+        zc, zn = zb[cur], zb[cur ^ 1]
+        ctx.surrogate_step(st, zc, k, S, zhat)
+        ctx.risk_update(st, wdc.PRE_DECISION, k, S)
+        t, tn = (S - k) / S, (S - k - 1) / S
+        ctx.forward(zc, t, dv["cond"], dv["text"], dv["cam"], out=v)
+        ctx.scheduler_step(zc, v, t, tn, out=zn)
+        ctx.risk_update(st, wdc.POST_EXACT, k, S, zc, zn)
+        return cur ^ 1
+
+    cur = exact_step(0, 0)
+    torch.cuda.synchronize()
+    ctx.set_timing(True)
+    t0 = time.perf_counter()
+    for k in range(1, steps + 1):
+        cur = exact_step(k, cur)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    tm = ctx.timing()
+    ctx.set_timing(False)
+    flops = cfg.flops_per_forward()
+    a_ms, a_n, a_work = tm["attention"]
+    g_ms, g_n, g_work = tm["gemm"]
+    out = {"workload": f"{name}-shaped world model: {cfg.n_blocks} sequential blocks, D={cfg.hidden}, "
+                       f"{cfg.heads}x{cfg.head_dim} heads, {cfg.n_video} video + {cfg.text_tokens} text tokens, "
+                       f"latent {'x'.join(map(str, cfg.latent))}",
+           "ms_per_exact_step": round(ms, 2), "tflops": round(flops / (ms / 1e3) / 1e12, 1),
+           "pct_bf16_peak": round(100.0 * flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+           "attention_ms_avg": round(a_ms / a_n, 3), "attention_tflops": round(a_work / (a_ms / 1e3) / 1e12, 1),
+           "linear_tflops": round(g_work / (g_ms / 1e3) / 1e12, 1)}
+    if RISK_TAU.get(name) is not None:
+        out["rollout_measured"] = rollout_leg(wdc, cfg, ctx, inp, torch, dev, tau=RISK_TAU[name])
+        out["rollout_measured"]["target_exact_ratio"] = TARGET_EXACT_RATIO[name]
+    del ctx, st, zb, zhat, v, dv
+    torch.cuda.empty_cache()
+    return out
 
 
 def stress_leg(wdc, synth, torch, dev, reps=3):
@@ -563,6 +622,9 @@ def main():
         out["rollout_periodic"] = rollout_leg(wdc, cfg, ctx, inp, torch, dev)
     del ctx, st, z, zbuf, zhat, v, cond, text, cam
     torch.cuda.empty_cache()
+    if not args.no_5b and args.workload == "13b":
+        log("5B-shaped exact steps and risk-controlled rollout ...")
+        out["workload_5b"] = second_workload_leg(wdc, synth, torch, dev)
     if not args.no_stress:
         log("118,800-token attention and single block ...")
         out["stress_118800"] = stress_leg(wdc, synth, torch, dev)
