@@ -15,7 +15,10 @@
 //    never goes through LDS;
 //  * softmax in base 2 against a per-row reference max, each step running the
 //    vector work of tile t + 1 inside the MFMA stream of tiles t and t + 2
-//    (k_attn_bf16_ppr3).
+//    (k_attn_bf16_ppr3);
+//  * one head's padded q, k and v^T rows are addressed with 32-bit byte
+//    offsets (buffer ranges, tile offsets): at most 2^30 B per head, which
+//    the library checks before launching (attn_len_ok).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
