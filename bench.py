@@ -510,6 +510,9 @@ def main():
     torch.cuda.synchronize()
 
     def exact_step(k, cur):
+        if k and k % S == 0:
+            st.reset()            # the schedule's S steps are used up: a new rollout
+        k %= S
         zc, zn = zbuf[cur], zbuf[cur ^ 1]
         ctx.surrogate_step(st, zc, k, S, zhat)
         ctx.risk_update(st, wdc.PRE_DECISION, k, S)
