@@ -64,3 +64,64 @@ def test_replay_rollout_on_unaligned_latent_twice_is_bitwise_identical():
         out.append((z, sched, logs))
     assert torch.equal(out[0][0], out[1][0]) and out[0][1] == out[1][1]
     _logs_equal(out[0][2], out[1][2])
+
+
+def _poisoned_context(wdc, torch, cfg, fill, params=None):
+    """A context whose workspace is a caller buffer with every byte ``fill``
+    (0xFF: float32 and bf16 NaN), weights bound later."""
+    ctx = wdc.Context(cfg, allocate_weights=False, params=params)
+    n = ctx.lib.wdc_workspace_bytes(ctx.h)
+    ctx.workspace = torch.full((n,), fill, dtype=torch.uint8, device="cuda")
+    ctx._check(ctx.lib.wdc_bind_workspace(ctx.h, ctx.workspace.data_ptr(), n))
+    return ctx
+
+
+def _poisoned_state(wdc, torch, ctx, fill):
+    import ctypes
+    st = wdc.State.__new__(wdc.State)
+    st.ctx = ctx
+    n = ctx.lib.wdc_state_bytes(ctx.h)
+    st.mem = torch.full((n,), fill, dtype=torch.uint8, device="cuda")
+    h = ctypes.c_void_p()
+    ctx._check(ctx.lib.wdc_state_create(ctx.h, ctypes.c_void_p(st.mem.data_ptr()), n, ctypes.byref(h)))
+    st.h = h
+    return st
+
+
+def test_results_do_not_depend_on_the_initial_contents_of_workspace_and_state():
+    """Workspace and rollout-state memory handed over full of NaN bytes give
+    the same bits as zero-filled ones: no kernel reads a scratch value, a
+    padding row or a bank slot before writing it (a bf16 forward with ragged
+    tiles and every block kind, and a float32 risk rollout)."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = small_cfg("bf16", latent=(16, 3, 10, 14))        # 105 video + 21 text tokens: partial tiles
+    outs = []
+    weights = None
+    for fill in (0x00, 0xFF):
+        ctx = _poisoned_context(wdc, torch, cfg, fill)
+        if weights is None:
+            weights = torch.empty(ctx.lib.wdc_weights_bytes(ctx.h), dtype=torch.uint8, device="cuda")
+            ctx.bind_weights(weights)
+            ctx.init_random_weights(seed=11, std=0.02)
+        else:
+            ctx.bind_weights(weights)
+        _, dv = dev_inputs(ctx, cfg)
+        outs.append(ctx.forward(dv["z_T"], 0.35, dv["cond"], dv["text"], dv["cam"]))
+    assert torch.isfinite(outs[0]).all() and torch.equal(outs[0], outs[1])
+
+    cfg = synth.get_config("tiny")
+    W = synth.gen_weights(cfg)
+    res = []
+    for fill in (0x00, 0xFF):
+        ctx = _poisoned_context(wdc, torch, cfg, fill, params=wdc.default_params(tau_risk=0.2))
+        ctx.weights = torch.zeros(ctx.lib.wdc_weights_bytes(ctx.h), dtype=torch.uint8, device="cuda")
+        ctx.bind_weights(ctx.weights)
+        ctx.load_weights(W)
+        _, dv = dev_inputs(ctx, cfg)
+        z = dv["z_T"].clone()
+        sched, logs = ctx.rollout(_poisoned_state(wdc, torch, ctx, fill), z, 8, dv["cond"], mode=wdc.MODE_RISK)
+        res.append((z, sched, logs))
+    assert 0 < sum(res[0][1]) < 8
+    assert torch.isfinite(res[0][0]).all() and torch.equal(res[0][0], res[1][0]) and res[0][1] == res[1][1]
+    _logs_equal(res[0][2], res[1][2])
