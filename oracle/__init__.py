@@ -1,7 +1,7 @@
 """CPU oracle for the WorldDynCache denoising rollout (test infrastructure).
 
 Plain, slow, float64 NumPy written from the paper. Only the test suite, the
-package's ``smoke()`` self-check and the benchmark's CPU-baseline leg may
+``__graft_entry__.smoke()`` self-check and the benchmark's CPU-baseline leg may
 import it; the GPU product path never does and shares no code with it (the
 only common module is ``synth``, which generates seeded inputs and holds none
 of the method's arithmetic).
