@@ -215,3 +215,32 @@ def _copy(dst_ptr, src_ptr, n):
     torch.cuda.synchronize()
     hip = C.CDLL("libamdhip64.so")
     assert hip.hipMemcpy(C.c_void_p(dst_ptr), C.c_void_p(src_ptr), C.c_size_t(4 * n), 3) == 0   # device to device
+
+
+@pytest.mark.parametrize("steps", [1, 2, 3])
+def test_short_rollouts_match_oracle(steps):
+    """The degenerate lengths: S = 1 (one exact step, nothing to reuse), S = 2
+    (the only step after the first is the last one) and S = 3, in every mode
+    (risk with an open threshold, forced surrogates everywhere, all exact,
+    periodic with period 2): schedule, logs and latent against the oracle."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    cfg = synth.get_config("tiny")
+    W = synth.gen_weights(cfg)
+    inp = synth.gen_inputs(cfg)
+    den = ro.dit_denoiser(W, cfg, inp)
+    cases = [("risk", wdc.MODE_RISK, dict(tau_risk=1e9), None),
+             ("forced", wdc.MODE_FORCED, {}, [1] * steps),
+             ("all_exact", wdc.MODE_ALL_EXACT, {}, None),
+             ("periodic", wdc.MODE_PERIODIC, dict(period=2), None)]
+    for name, mode, over, forced in cases:
+        ref = ro.rollout(den, inp["z_T"], steps, P.with_(P.DEFAULTS, **over), mode=name, forced=forced)
+        ctx = context(cfg, params=wdc.default_params(**over))
+        _, dv = dev_inputs(ctx, cfg)
+        z = dv["z_T"].clone()
+        sched, logs = ctx.rollout(ctx.new_state(), z, steps, dv["cond"], mode=mode, forced=forced)
+        print(f"S={steps} {name}: schedule {sched} oracle {ref.schedule}")
+        assert sched == ref.schedule and sched[0] == 0, name
+        for g, o in zip(logs, ref.log):
+            compare_logs(g, o, 1e-4)
+        assert rel_l2(z.cpu().numpy(), ref.z) <= TOL_F32, name
