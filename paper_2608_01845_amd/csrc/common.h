@@ -52,6 +52,24 @@ __device__ __forceinline__ double warp_sum_d(double v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+// Sum over each aligned group of G consecutive lanes (G = 8 or 16) with DPP
+// lane moves, no LDS round trip: lane pairs (quad permutation 1 0 3 2), pairs
+// of pairs (2 3 0 1), quads (mirror within 8 lanes), halves of 16 (mirror
+// within 16). After each step the two partners hold a + b and b + a, the same
+// bits, so every lane of a group ends with the same sum.
+template <int DPP_CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), DPP_CTRL, 0xF, 0xF, false));
+}
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(G == 8 || G == 16, "group of 8 or 16 lanes");
+  v += dpp_move<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_move<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_move<0x141>(v);  // row_half_mirror
+  if (G == 16) v += dpp_move<0x140>(v);  // row_mirror
+  return v;
+}
 __device__ __forceinline__ float warp_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

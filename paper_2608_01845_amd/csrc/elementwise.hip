@@ -191,11 +191,8 @@ __global__ __launch_bounds__(256) void k_qk_prep8(QKVPrepArgs a) {
       sq += q[e] * q[e];
       sk += k[e] * k[e];
     }
-#pragma unroll
-    for (int o = TPH / 2; o > 0; o >>= 1) {
-      sq += __shfl_xor(sq, o, 64);
-      sk += __shfl_xor(sk, o, 64);
-    }
+    sq = group_sum<TPH>(sq);
+    sk = group_sum<TPH>(sk);
     const float rq = rsqrtf(sq / (float)HD + 1e-6f), rk = rsqrtf(sk / (float)HD + 1e-6f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {

@@ -190,53 +190,83 @@ __device__ __forceinline__ const char *qkv_chunk(const char *smem, int row, int 
 // whole head rows. HD / 8 consecutive lanes hold one head row. The arithmetic
 // is that of the separate preparation kernel (k_qk_prep8), without fused
 // multiply-adds in either, so both give the same bits.
-template <int HD>
+template <int HD, bool ROPE>
 __device__ __forceinline__ void qk_scatter(const GemmArgs &g, const char *smem, int64_t m0, int h0, bf16_t *dst) {
 #pragma clang fp contract(off)
   const QkvOut &o = g.qkv;
   constexpr int TPH = HD / 8;
-  // iteration it handles tile row 16 it + threadIdx.x / 32 (chunk threadIdx.x % 32);
-  // its sample and token advance incrementally (no division per row)
+  // Iteration it handles tile row 16 it + threadIdx.x / 32; the thread's chunk
+  // of the row (threadIdx.x % 32: head hh, eight columns from 8 c) is the same
+  // in every iteration. The sample and token advance incrementally (no
+  // division per row). With a rotation table (ROPE: a table and video rows)
+  // its entries go out four rows at a time, one group of four ahead, and
+  // unconditionally (rows that take no rotation read table row 0), so the
+  // stores of a group never stand between a table read and its use.
+  const int cc = threadIdx.x & 31, hh = cc / TPH, c = cc % TPH;
   const int64_t r_first = m0 + (threadIdx.x >> 5);
   int64_t b = (int64_t)blockIdx.z + r_first / o.rps, jr = r_first % o.rps;
-  // (unrolled by 4: the rotation table loads of four rows are in flight together)
-#pragma unroll 4
-  for (int it = 0; it < 16; ++it) {
-    const int cg = it * 512 + threadIdx.x, row = cg >> 5, cc = cg & 31;
-    const int hh = cc / TPH, c = cc % TPH;
-    const int64_t r = m0 + row;
-    const int64_t bs = b, j = o.row0 + jr;
-    jr += 16;
-    while (jr >= o.rps) {
-      jr -= o.rps;
-      ++b;
-    }
-    float x[8];
-    unpack8(*(const uint4 *)qkv_chunk(smem, row, cc), x);
-    if (o.qk_norm) {
-      float sq = 0.f;
+  int64_t bsv[2][4], jv[2][4];   // group g4 in slot g4 & 1
+  float4 cs4v[2][4][2];
+  auto rotates = [&](int it, int64_t jt) { return ROPE && jt < o.n_video && m0 + 16 * it + (threadIdx.x >> 5) < g.m; };
+  auto coords = [&](int64_t (&bs4)[4], int64_t (&j4)[4]) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sq += x[e] * x[e];
-#pragma unroll
-      for (int off = TPH / 2; off > 0; off >>= 1) sq += __shfl_xor(sq, off, 64);
-      const float rs = rsqrtf(sq / (float)HD + 1e-6f);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] *= rs;
-    }
-    if (r >= g.m) continue;
-    if (o.rope && j < o.n_video) {
-      const float4 *cs4 = (const float4 *)(o.rope + j * (HD / 2) + 4 * c);
-      const float4 c01 = cs4[0], c23 = cs4[1];
-      const float cs[8] = {c01.x, c01.y, c01.z, c01.w, c23.x, c23.y, c23.z, c23.w};
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const float co = cs[2 * p], si = cs[2 * p + 1];
-        const float t0 = x[2 * p] * co - x[2 * p + 1] * si, t1 = x[2 * p] * si + x[2 * p + 1] * co;
-        x[2 * p] = t0;
-        x[2 * p + 1] = t1;
+    for (int u = 0; u < 4; ++u) {
+      bs4[u] = b;
+      j4[u] = o.row0 + jr;
+      jr += 16;
+      while (jr >= o.rps) {
+        jr -= o.rps;
+        ++b;
       }
     }
-    *(uint4 *)(dst + ((bs * o.heads + h0 + hh) * o.n_pad + j) * HD + 8 * c) = pack8(x);
+  };
+  auto fetch = [&](int g4, const int64_t (&js)[4], float4 (&dst4)[4][2]) {
+    if (!ROPE) return;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t jt = rotates(4 * g4 + u, js[u]) ? js[u] : 0;
+      const float4 *cs4 = (const float4 *)(o.rope + jt * (HD / 2) + 4 * c);
+      dst4[u][0] = cs4[0];
+      dst4[u][1] = cs4[1];
+    }
+  };
+  coords(bsv[0], jv[0]);
+  fetch(0, jv[0], cs4v[0]);
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int sl = g4 & 1;
+    if (g4 + 1 < 4) {
+      coords(bsv[sl ^ 1], jv[sl ^ 1]);
+      fetch(g4 + 1, jv[sl ^ 1], cs4v[sl ^ 1]);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int it = 4 * g4 + u, row = 16 * it + (threadIdx.x >> 5);
+      float x[8];
+      unpack8(*(const uint4 *)qkv_chunk(smem, row, cc), x);
+      if (o.qk_norm) {
+        float sq = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sq += x[e] * x[e];
+        sq = group_sum<TPH>(sq);
+        const float rs = rsqrtf(sq / (float)HD + 1e-6f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] *= rs;
+      }
+      if (m0 + row >= g.m) continue;
+      if (rotates(it, jv[sl][u])) {
+        const float4 c01 = cs4v[sl][u][0], c23 = cs4v[sl][u][1];
+        const float cs[8] = {c01.x, c01.y, c01.z, c01.w, c23.x, c23.y, c23.z, c23.w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const float co = cs[2 * p], si = cs[2 * p + 1];
+          const float t0 = x[2 * p] * co - x[2 * p + 1] * si, t1 = x[2 * p] * si + x[2 * p + 1] * co;
+          x[2 * p] = t0;
+          x[2 * p + 1] = t1;
+        }
+      }
+      *(uint4 *)(dst + ((bsv[sl][u] * o.heads + h0 + hh) * o.n_pad + jv[sl][u]) * HD + 8 * c) = pack8(x);
+    }
   }
 }
 
@@ -573,10 +603,14 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
       const int region = (int)(n0 / g.qkv.d), h0 = (int)((n0 % g.qkv.d) / g.qkv.hd);
       if (region < 2) {
         bf16_t *dst = (bf16_t *)(region == 0 ? g.qkv.q : g.qkv.k);
-        if (g.qkv.hd == 128)
-          qk_scatter<128>(g, smem, m0, h0, dst);
-        else
-          qk_scatter<64>(g, smem, m0, h0, dst);
+        const bool rope = g.qkv.rope && g.qkv.n_video > 0;
+        if (g.qkv.hd == 128) {
+          if (rope) qk_scatter<128, true>(g, smem, m0, h0, dst);
+          else qk_scatter<128, false>(g, smem, m0, h0, dst);
+        } else {
+          if (rope) qk_scatter<64, true>(g, smem, m0, h0, dst);
+          else qk_scatter<64, false>(g, smem, m0, h0, dst);
+        }
       } else if (g.qkv.hd == 128) {
         v_scatter<128>(g, smem, m0, h0);
       } else {
