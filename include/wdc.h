@@ -294,10 +294,23 @@ wdc_status wdc_rollout_batch(wdc_ctx *ctx, wdc_state *const *states, int32_t B, 
  * [h*hd, (h+1)*hd); ldo >= heads*hd (else WDC_E_ARG). q, k, vt 16-byte
  * aligned; for bf16 d_o 8-byte aligned and ldo a multiple of 4 (else
  * WDC_E_ALIGN); bf16 with n_pad * hd * 2 above 2^30 bytes (32-bit offsets
- * within a head) is WDC_E_SHAPE. */
+ * within a head) is WDC_E_SHAPE. bf16 may use the bound workspace as scratch
+ * (wdc_attention_plan), so q, k, vt and o must not lie in it. */
 int64_t wdc_attn_pad(int64_t n);
 wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const void *d_vt, int64_t n, void *d_o,
                          int64_t ldo);
+/* How the bf16 attention of this context runs n tokens (one sample, the
+ * context's heads): query blocks of 256 per head that run over all keys
+ * (*qb_main), and the number of key ranges (*kv_splits, 1 = none) each of
+ * the remaining blocks of the last, partly filled dispatch round runs as;
+ * those ranges are combined by a second launch. A split uses the bound
+ * workspace's projection area as scratch (its contents are not kept), so
+ * without a workspace, or when it is too small, *kv_splits is 1. The
+ * environment variable WDC_ATTN_SPLITS, read at wdc_create, overrides the
+ * estimate (1: never split; s >= 2: s ranges whenever a round is partial,
+ * at most one per key tile). Float32 contexts: *qb_main = every block,
+ * *kv_splits = 1. Either output may be NULL. */
+wdc_status wdc_attention_plan(const wdc_ctx *ctx, int64_t n, int32_t *qb_main, int32_t *kv_splits);
 
 /* c[m, n] = sum_k a[m, k] * w[n, k] + bias[n] in the model dtype with float32
  * accumulation; a row stride lda, c row stride ldc. */

@@ -119,6 +119,7 @@ def load() -> C.CDLL:
                                     C.POINTER(C.c_uint8), C.POINTER(StepLog)]),
         "wdc_attn_pad": (i64, [i64]),
         "wdc_attention": (i32, [vp, vp, vp, vp, i64, vp, i64]),
+        "wdc_attention_plan": (i32, [vp, i64, C.POINTER(i32), C.POINTER(i32)]),
         "wdc_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, i64, i64]),
         "wdc_set_timing": (i32, [vp, i32]),
         "wdc_timing": (i32, [vp, C.POINTER(dbl), C.POINTER(i64), C.POINTER(dbl)]),
@@ -137,8 +138,8 @@ def exported_symbols() -> List[str]:
         "wdc_weight_info", "wdc_bind_weights", "wdc_init_weights_random", "wdc_workspace_bytes", "wdc_bind_workspace",
         "wdc_state_bytes", "wdc_state_create", "wdc_state_reset", "wdc_state_destroy", "wdc_state_bank_slot",
         "wdc_cond_embed", "wdc_dit_block_forward", "wdc_dit_forward", "wdc_dit_forward_batch", "wdc_scheduler_step",
-        "wdc_surrogate_step", "wdc_surrogate_step_noalloc", "wdc_risk_update", "wdc_rollout", "wdc_rollout_batch", "wdc_attn_pad", "wdc_attention", "wdc_linear", "wdc_set_timing",
-        "wdc_timing"]
+        "wdc_surrogate_step", "wdc_surrogate_step_noalloc", "wdc_risk_update", "wdc_rollout", "wdc_rollout_batch", "wdc_attn_pad", "wdc_attention", "wdc_attention_plan", "wdc_linear",
+        "wdc_set_timing", "wdc_timing"]
 
 
 class WdcError(RuntimeError):
@@ -309,6 +310,12 @@ class Context:
 
     def attn_pad(self, n: int) -> int:
         return self.lib.wdc_attn_pad(n)
+
+    def attention_plan(self, n: int):
+        """(query blocks per head over all keys, key ranges of each remaining block)."""
+        qb, ks = C.c_int32(), C.c_int32()
+        self._check(self.lib.wdc_attention_plan(self.h, n, C.byref(qb), C.byref(ks)))
+        return qb.value, ks.value
 
     def linear(self, a, w, bias, out, m: int, n: int, k: int, lda: int = None, ldc: int = None):
         self._check(self.lib.wdc_linear(self.h, _ptr(a), lda or k, _ptr(w), _ptr(bias), _ptr(out), ldc or n, m, n, k))

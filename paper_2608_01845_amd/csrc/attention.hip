@@ -22,6 +22,9 @@
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
+#include <algorithm>
+#include <numeric>
+
 namespace wdc {
 
 int64_t attn_pad(int64_t n) { return ((n + 255) / 256) * 256; }
@@ -212,6 +215,73 @@ __device__ __forceinline__ float ppr_exp(const f32x16 (&S)[2], bf16x8 (&pf)[4]) 
   return ls;
 }
 
+// End of a key-range block (block j of the split round: head h, query block
+// qb_main + qt, range sp, in that nesting): its unnormalised rows O (float32),
+// reference maxima m and row sums l go to slot (j * 256 + query) of the
+// scratch: O at part + slot * HD, (m, l) at part + slots * HD + 2 slot.
+template <int HD>
+__device__ __forceinline__ void attn_split_store(const AttnArgs &a, const f32x16 (&o)[HD / 32], float m, float lt,
+                                                 int j) {
+  const int lane = threadIdx.x & 63, lr = lane & 31, lg = lane >> 5, wid = threadIdx.x >> 6;
+  const int tail = (int)(a.n_pad / 256) - a.qb_main;
+  const int64_t slots = (int64_t)a.heads * tail * a.kv_splits * 256;
+  const int64_t slot = (int64_t)j * 256 + wid * 32 + lr;
+  float *po = a.part + slot * HD;
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      *(float4 *)(po + 32 * i + 8 * g4 + 4 * lg) =
+          make_float4(o[i][4 * g4], o[i][4 * g4 + 1], o[i][4 * g4 + 2], o[i][4 * g4 + 3]);
+  if (lg == 0) *(float2 *)(a.part + slots * HD + 2 * slot) = make_float2(m, lt);
+}
+
+// Combine of the split round, after the attention launch: for each of its
+// queries (thread: one query, eight columns) the key ranges in range order,
+//   O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,  M = max_s m_s
+// (m in log2 units), rounded to bf16 once.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  constexpr int C8 = HD / 8;
+  const int ns = a.kv_splits, tail = (int)(a.n_pad / 256) - a.qb_main;
+  const int64_t slots = (int64_t)a.heads * tail * ns * 256;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (int64_t)a.heads * tail * 256 * C8) return;
+  const int c8 = (int)(gid % C8);
+  const int64_t qt = gid / C8;                   // (head, tail query block, query)
+  const int qi = (int)(qt % 256);
+  const int64_t hb = qt / 256;                   // head * tail + tail query block
+  const int h = (int)(hb / tail), qb = a.qb_main + (int)(hb % tail);
+  const int64_t q = (int64_t)qb * 256 + qi;
+  if (q >= a.n) return;
+  const int64_t s0 = hb * ns * 256 + qi;         // slot of range 0; range r at s0 + 256 r
+  const float *pml = a.part + slots * HD;
+  float mx = -INFINITY;
+  for (int r = 0; r < ns; ++r) mx = fmaxf(mx, pml[2 * (s0 + 256 * r)]);
+  float den = 0.f, acc[8] = {};
+  for (int r = 0; r < ns; ++r) {
+    const int64_t sl = s0 + 256 * r;
+    const float w = __builtin_amdgcn_exp2f(pml[2 * sl] - mx);
+    den += w * pml[2 * sl + 1];
+    const float4 v0 = *(const float4 *)(a.part + sl * HD + 8 * c8);
+    const float4 v1 = *(const float4 *)(a.part + sl * HD + 8 * c8 + 4);
+    acc[0] += w * v0.x;
+    acc[1] += w * v0.y;
+    acc[2] += w * v0.z;
+    acc[3] += w * v0.w;
+    acc[4] += w * v1.x;
+    acc[5] += w * v1.y;
+    acc[6] += w * v1.z;
+    acc[7] += w * v1.w;
+  }
+  const float inv = 1.f / den;
+  bf16_t *O = (bf16_t *)a.o + out_off(a, h, q, HD) + 8 * c8;
+  *(uint2 *)O = make_uint2((uint32_t)f2bf(acc[0] * inv) | ((uint32_t)f2bf(acc[1] * inv) << 16),
+                           (uint32_t)f2bf(acc[2] * inv) | ((uint32_t)f2bf(acc[3] * inv) << 16));
+  *(uint2 *)(O + 4) = make_uint2((uint32_t)f2bf(acc[4] * inv) | ((uint32_t)f2bf(acc[5] * inv) << 16),
+                                 (uint32_t)f2bf(acc[6] * inv) | ((uint32_t)f2bf(acc[7] * inv) << 16));
+}
+
 // bf16 flash attention. 8 wavefronts per block (two per SIMD), 32 queries each
 // (256 per block); K tiles of 64 keys and V^T tiles reach four K and four V^T
 // LDS slots by direct buffer loads issued by waves 0-3; one block barrier per
@@ -235,13 +305,31 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
   using TL = TileLoad<HD>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
-  int h = blockIdx.y, qb = blockIdx.x;
-  if (a.xcd_order) {
-    const int id = blockIdx.x + blockIdx.y * gridDim.x;
-    const int li = id >> 3;
-    h = (id & 7) + 8 * (li / gridDim.x);
-    qb = li % gridDim.x;
+  // Block b < heads x qb_main: query block qb < qb_main of head h over all
+  // keys (with the XCD order, each XCD runs whole heads: blocks go to the XCDs
+  // round robin); the rest: query block qb >= qb_main of head h, key range sp
+  // of kv_splits, in (head, query block, range) order.
+  const int ns = a.kv_splits > 1 ? a.kv_splits : 1;
+  const int nqb = (int)(a.n_pad / QB), tail = nqb - a.qb_main;
+  const int bid = blockIdx.x, main_blocks = a.heads * a.qb_main;
+  int h, qb, sp = 0, nr = 1;                  // key range sp of nr
+  if (bid < main_blocks) {
+    if (a.xcd_order) {
+      const int li = bid >> 3;
+      h = (bid & 7) + 8 * (li / a.qb_main);
+      qb = li % a.qb_main;
+    } else {
+      h = bid / a.qb_main;
+      qb = bid % a.qb_main;
+    }
+  } else {
+    const int j = bid - main_blocks;
+    h = j / (tail * ns);
+    qb = a.qb_main + (j % (tail * ns)) / ns;
+    sp = j % ns;
+    nr = ns;
   }
+
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool grp_a = wid < 4;
@@ -258,10 +346,22 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
     for (int j = 0; j < 8; ++j) qf[s][j] = (__bf16)((float)raw[j] * sc);
   }
 
+  // key tiles [t_first, t_first + ntiles) of tiles_all (all of them outside
+  // the split round); only the range that ends the sequence holds the partial
+  // last tile. The K and V^T buffer ranges start at the range's first key, so
+  // the tile loads address tiles relative to the range.
+  const int tiles_all = (int)((a.n + KV - 1) / KV);
+  const int t_first = (int)((int64_t)sp * tiles_all / nr);
+  const int t_end = (int)((int64_t)(sp + 1) * tiles_all / nr);
+  const int ntiles = t_end - t_first;
+  const int last_valid = t_end == tiles_all ? (int)(a.n - (int64_t)(tiles_all - 1) * KV) : KV;
+  const int64_t key0 = (int64_t)t_first * KV;
   const __amdgpu_buffer_rsrc_t kdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.k + (int64_t)h * a.n_pad * HD), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+      (void *)((const bf16_t *)a.k + ((int64_t)h * a.n_pad + key0) * HD), (short)0,
+      (int)((a.n_pad - key0) * HD * 2), RSRC_WORD3);
   const __amdgpu_buffer_rsrc_t vdesc = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad), (short)0, (int)(a.n_pad * HD * 2), RSRC_WORD3);
+      (void *)((const bf16_t *)a.v + (int64_t)h * HD * a.n_pad + key0), (short)0,
+      (int)((a.n_pad * HD - key0) * 2), RSRC_WORD3);
   const int lw = wid & 3;
   const TileLoad<HD> tl(lw, lane, a.n_pad);
   int kro[HD / 16];
@@ -271,8 +371,6 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) vro[j] = V_BASE + vslot(lr, 2 * j + lg);
 
-  const int ntiles = (int)((a.n + KV - 1) / KV);
-  const int last_valid = (int)(a.n - (int64_t)(ntiles - 1) * KV);
   auto load_k = [&](int b, int tile) {
 #pragma unroll
     for (int i = 0; i < TL::K_STRIPES; ++i)
@@ -463,6 +561,10 @@ __global__ __launch_bounds__(512, 1) void k_attn_bf16_ppr3(AttnArgs a) {
 #undef WDC_PPR3_READ
 
   const float lt = l + __shfl_xor(l, 32, 64);
+  if (bid >= main_blocks && ns > 1) {
+    attn_split_store<HD>(a, o, m, lt, bid - main_blocks);
+    return;
+  }
   const float inv = 1.f / lt;
   const int64_t q = qbase + lr;
   if (q < a.n) {
@@ -487,12 +589,61 @@ hipError_t launch_bf16_ppr3(const AttnArgs &a, hipStream_t s) {
     const hipError_t e = hipFuncSetAttribute((const void *)k_attn_bf16_ppr3<HD>, hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
     if (e != hipSuccess) return e;
   }
-  dim3 grid((unsigned)((a.n + 255) / 256), (unsigned)a.heads);
-  hipLaunchKernelGGL((k_attn_bf16_ppr3<HD>), grid, dim3(512), LDS, s, a);
+  AttnArgs b = a;
+  attn_split_plan(b);
+  const int nqb = (int)(b.n_pad / 256);
+  const int64_t blocks = (int64_t)b.heads * b.qb_main + (int64_t)b.heads * (nqb - b.qb_main) * b.kv_splits;
+  hipLaunchKernelGGL((k_attn_bf16_ppr3<HD>), dim3((unsigned)blocks), dim3(512), LDS, s, b);
+  if (b.kv_splits > 1) {
+    const int64_t items = (int64_t)b.heads * (nqb - b.qb_main) * 256 * (HD / 8);
+    hipLaunchKernelGGL((k_attn_combine<HD>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, b);
+  }
   return hipGetLastError();
 }
 
 }  // namespace
+
+// Key-range split of the last dispatch round. Query blocks [0, qb_main) of
+// every head fill whole rounds (heads x qb_main a multiple of the compute
+// units); the other heads x (nqb - qb_main) blocks would leave CUs idle in a
+// partial round, so each runs as s blocks over s disjoint key ranges when the
+// estimate says so: ceil(tail s / CUs) / s rounds of a block's time, against
+// ceil(tail / CUs), plus the scratch traffic (written once, read once). A
+// block's time is taken at about half the bf16 peak of one CU; at least 8
+// key tiles per range.
+void attn_split_plan(AttnArgs &b) {
+  const int nqb = (int)(b.n_pad / 256);
+  b.qb_main = nqb;
+  b.kv_splits = 1;
+  const int cus = device_cus();
+  if (!b.part || b.force_splits == 1 || cus <= 0) return;
+  const int g = cus / std::gcd(cus, b.heads);    // heads x g blocks fill whole rounds
+  const int qb_main = nqb / g * g, tail = nqb - qb_main;
+  const int64_t tb = (int64_t)b.heads * tail;
+  if (tail == 0) return;
+  const int tiles = (int)((b.n + 63) / 64);
+  auto bytes = [&](int s) { return (size_t)(tb * s * 256) * (size_t)(b.hd + 2) * sizeof(float); };
+  int best_s = 1;
+  if (b.force_splits >= 2) {
+    best_s = std::min(b.force_splits, tiles);
+    if (bytes(best_s) > b.part_bytes) return;
+  } else {
+    const double t_blk = 1024.0 * (double)b.n * b.hd / 4.9e12;
+    const double base = (double)((tb + cus - 1) / cus) * t_blk;
+    double best = base;
+    for (int s = 2; s <= 8 && tiles >= 8 * s && bytes(s) <= b.part_bytes; ++s) {
+      const double t = (double)((tb * s + cus - 1) / cus) / s * t_blk + 2.0 * (double)bytes(s) / 4e12;
+      if (t < best) {
+        best = t;
+        best_s = s;
+      }
+    }
+    if (best >= 0.9 * base) best_s = 1;
+  }
+  if (best_s < 2) return;
+  b.qb_main = qb_main;
+  b.kv_splits = best_s;
+}
 
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;

@@ -156,6 +156,9 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g, hipStream_t s);
 // kernels, the only ones with the EPI_QKV epilogue.
 bool gemm_qkv_fusable(int dtype, const GemmArgs &g);
 
+// compute units of the current device (0 if the query fails)
+int device_cus();
+
 // True the first time it is called with this flag array on the current device
 // (kernel attributes such as the dynamic LDS limit are set per device). A
 // device id outside the array, or a failed query, always answers true.
@@ -178,11 +181,24 @@ struct AttnArgs {
   // (sample h / hpb, head h % hpb), whose rows start at sample * n in o;
   // 0 = one sample
   int hpb;
+  // Scratch for splitting the key range of the last, partly filled dispatch
+  // round (bf16): part (part_bytes) takes each key range's unnormalised rows,
+  // reference maxima and row sums until a second launch combines them. Null:
+  // no split.
+  float *part;
+  size_t part_bytes;
+  int force_splits;       // 0: by the cost estimate; 1: never split; s >= 2: s splits whenever a round is partial
+  // set by launch_attention: query blocks per head that run over all keys
+  // (the rest run as kv_splits key ranges each)
+  int qb_main, kv_splits;
 };
 int64_t attn_pad(int64_t n);
 // The bf16 attention kernel addresses one head's padded rows of q, k and v^T
 // with 32-bit byte offsets (buffer ranges, tile offsets): keep a head within 2^30 B.
 inline bool attn_len_ok(int64_t n, int hd) { return attn_pad(n) * hd * 2 <= (int64_t(1) << 30); }
+// Sets qb_main and kv_splits of a bf16 launch (every query block over all
+// keys unless the scratch allows and the estimate favours a split).
+void attn_split_plan(AttnArgs &a);
 hipError_t launch_attention(int dtype, const AttnArgs &a, hipStream_t s);
 
 // ------------------------------------------------------------------ elementwise and small kernels

@@ -20,6 +20,16 @@
 
 namespace wdc {
 
+// compute units of the current device (the rectangle order needs exactly 256)
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus[dev] = 0;
+  return cus[dev];
+}
+
 namespace {
 
 template <typename T>
@@ -722,16 +732,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(GemmArgs g0) {
 #undef WDC_GEMM_READ
 #undef WDC_GEMM_BARRIER
 #undef WDC_GEMM_LOAD
-}
-
-// compute units of the current device (the rectangle order needs exactly 256)
-int device_cus() {
-  static int cus[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (!cus[dev] && hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    cus[dev] = 0;
-  return cus[dev];
 }
 
 template <int BM, int BN, int WM, int WN>

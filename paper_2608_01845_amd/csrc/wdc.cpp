@@ -64,6 +64,11 @@ struct wdc_ctx {
   // 128 x 128 tiles (WDC_FILL_TILES=0: tile size by shape alone, so tests can
   // reach the 256 x 256 kernels and the fused q/k/v epilogue at small sizes)
   bool fill_tiles = true;
+  // key-range split of the attention's last partial dispatch round
+  // (WDC_ATTN_SPLITS: unset or 0 by the cost estimate, 1 never, s >= 2 always
+  // s ranges, for tests)
+  int attn_splits = 0;
+  size_t qkv_bytes = 0;  // the projection buffer, scratch of the split attention
   // timing
   bool timing = false;
   std::vector<TimedEvent> events;
@@ -327,6 +332,14 @@ wdc_status mod_gemv(wdc_ctx *c, const std::string &name, int64_t off) {
   return WDC_OK;
 }
 
+// The projection buffer is free while attention runs (q, k and v^T are in
+// their own buffers by then): scratch for the split of the last round.
+void attn_scratch(wdc_ctx *c, AttnArgs &a) {
+  a.part = c->ws ? (float *)c->qkv : nullptr;
+  a.part_bytes = c->ws ? c->qkv_bytes : 0;
+  a.force_splits = c->attn_splits;
+}
+
 // joint attention of every sample: q/k/v hold nb x H heads, O rows follow the samples
 wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
   const int hb = c->H * c->nb;
@@ -342,6 +355,7 @@ wdc_status attention(wdc_ctx *c, void *o, int64_t ldo) {
   a.heads = hb;
   a.hd = c->hd;
   a.hpb = c->H;
+  attn_scratch(c, a);
   const double aw = 4.0 * (double)c->n * (double)c->n * c->hd * hb;
   HIPCHK(c, timed(c, WDC_T_ATTENTION, aw, [&] { return launch_attention(c->d.dtype, a, c->stream); }));
   return WDC_OK;
@@ -1118,6 +1132,7 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
   c->mb = d.max_batch > 1 ? d.max_batch : 1;
   c->fuse_qkv = !(getenv("WDC_FUSE_QKV") && atoi(getenv("WDC_FUSE_QKV")) == 0);
   c->fill_tiles = !(getenv("WDC_FILL_TILES") && atoi(getenv("WDC_FILL_TILES")) == 0);
+  c->attn_splits = getenv("WDC_ATTN_SPLITS") ? std::max(0, atoi(getenv("WDC_ATTN_SPLITS"))) : 0;
   c->stream = (hipStream_t)stream;
   c->esz = d.dtype == WDC_BF16 ? 2 : 4;
   c->D = d.hidden;
@@ -1216,6 +1231,7 @@ wdc_status wdc_bind_workspace(wdc_ctx *ctx, void *d_ws, size_t bytes) {
   ctx->x = (float *)(b + L.x);
   ctx->h = b + L.h;
   ctx->qkv = b + L.qkv;
+  ctx->qkv_bytes = L.cat - L.qkv;
   ctx->cat = b + L.cat;
   ctx->q = b + L.q;
   ctx->k = b + L.k;
@@ -1568,8 +1584,28 @@ wdc_status wdc_attention(wdc_ctx *ctx, const void *d_q, const void *d_k, const v
   a.ldo = ldo;
   a.heads = ctx->H;
   a.hd = ctx->hd;
+  attn_scratch(ctx, a);
   const double aw = 4.0 * (double)n * (double)n * ctx->hd * ctx->H;
   HIPCHK(ctx, timed(ctx, WDC_T_ATTENTION, aw, [&] { return launch_attention(ctx->d.dtype, a, ctx->stream); }));
+  return WDC_OK;
+}
+
+wdc_status wdc_attention_plan(const wdc_ctx *ctx, int64_t n, int32_t *qb_main, int32_t *kv_splits) {
+  if (!ctx || n <= 0) return WDC_E_ARG;
+  AttnArgs a{};
+  a.n = n;
+  a.n_pad = attn_pad(n);
+  a.heads = ctx->H;
+  a.hd = ctx->hd;
+  attn_scratch(const_cast<wdc_ctx *>(ctx), a);
+  if (ctx->d.dtype == WDC_BF16) {
+    attn_split_plan(a);
+  } else {
+    a.qb_main = (int)(a.n_pad / 256);
+    a.kv_splits = 1;
+  }
+  if (qb_main) *qb_main = a.qb_main;
+  if (kv_splits) *kv_splits = a.kv_splits;
   return WDC_OK;
 }
 

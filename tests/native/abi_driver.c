@@ -142,6 +142,11 @@ static void host_checks(void) {
     EXPECT(end <= wdc_weights_bytes(ctx), "weights blob too small");
     EXPECT(wdc_weight_info(ctx, n, NULL, NULL, NULL, NULL) != WDC_OK, "tensor index past the end accepted");
     EXPECT(wdc_workspace_bytes(ctx) > 0 && wdc_state_bytes(ctx) > 0, "sizes");
+    /* no workspace bound: no scratch, so no key-range split */
+    int32_t qbm = -1, ks = -1;
+    OK(wdc_attention_plan(ctx, 67576, &qbm, &ks));
+    EXPECT(qbm == 264 && ks == 1, "attention plan without a workspace: %d blocks, %d ranges", (int)qbm, (int)ks);
+    EXPECT(wdc_attention_plan(ctx, 0, &qbm, &ks) == WDC_E_ARG, "empty attention plan accepted");
     /* calls before weights and workspace are bound fail cleanly */
     float dummy = 0.f;
     EXPECT(wdc_dit_forward(ctx, &dummy, 0.5, NULL, NULL, NULL, &dummy) != WDC_OK, "unbound forward accepted");
@@ -169,6 +174,7 @@ static void host_checks(void) {
   EXPECT(wdc_create(&good, &q, NULL, &ctx) == WDC_E_ARG, "bank capacity past the maximum accepted");
   EXPECT(wdc_create(NULL, &p, NULL, &ctx) == WDC_E_ARG, "null descriptor accepted");
   EXPECT(wdc_destroy(NULL) != WDC_OK, "null context accepted");
+  EXPECT(wdc_attention_plan(NULL, 10, NULL, NULL) == WDC_E_ARG, "attention plan of a null context accepted");
   EXPECT(wdc_weights_bytes(NULL) == 0 && wdc_weight_count(NULL) == 0, "null context sizes");
 }
 
@@ -330,6 +336,10 @@ static void gpu_checks(void) {
   float *q = (float *)dev_fill((size_t)d.heads * np * d.head_dim), *o = NULL;
   HIPOK(hipMalloc((void **)&o, (size_t)N * d.hidden * sizeof(float)));
   OK(wdc_attention(ctx, q, q, q, N, o, d.hidden));
+  int32_t qbm = -1, ks = -1;
+  OK(wdc_attention_plan(ctx, N, &qbm, &ks));
+  EXPECT(qbm >= 0 && qbm <= (int32_t)(np / 256) && ks >= 1 && ks <= 8, "attention plan %d blocks, %d ranges", (int)qbm,
+         (int)ks);
   EXPECT(wdc_attention(ctx, q, q, q, N, o, d.hidden - 1) == WDC_E_ARG, "overlapping output rows accepted");
   EXPECT(wdc_attention(ctx, (const char *)q + 4, q, q, N, o, d.hidden) == WDC_E_ALIGN, "misaligned q accepted");
   OK(wdc_linear(ctx, x, d.hidden, w, NULL, o, d.hidden, N, d.hidden, d.hidden));
