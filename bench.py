@@ -27,11 +27,12 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0
-# HBM traffic per launch of the dominant kernel from two rocprofv3 --pmc passes
-# (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, scale factors from a 1 GiB device
-# copy; profiles/attention_13b_hbm_traffic.md). Valid only for the kernel
-# version named here; set to None whenever that kernel changes.
-MEASURED_TRAFFIC = {"k_attn_bf16_ppr3<128>": 8.306e9}
+# HBM traffic per attention call of the dominant kernel from two rocprofv3
+# --pmc passes (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, scale factors from a
+# 1 GiB device copy; profiles/attention_13b_hbm_traffic.md): the attention
+# kernel plus the combine launch of its split last round. Valid only for the
+# kernel version named here; set to None whenever that kernel changes.
+MEASURED_TRAFFIC = {"k_attn_bf16_ppr3<128>": 9.386e9}
 ATTN_KERNEL = {128: "k_attn_bf16_ppr3<128>", 64: "k_attn_bf16_ppr3<64>"}   # default bf16 kernel by head size
 METRIC = "DiT fwd TFLOP/s (% bf16 MFMA peak) + denoising steps/s at 13B shape"
 # Risk thresholds (Eq. (10)) of the measured rollouts, one per workload, for the
@@ -611,7 +612,7 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
                      "traffic": MEASURED_TRAFFIC.get(ATTN_KERNEL.get(cfg.head_dim)) if args.workload == "13b" else None,
-                     "traffic_unit": "bytes per launch"},
+                     "traffic_unit": "bytes per attention call (attention kernel + combine)"},
     }
     if not args.no_rollout and RISK_TAU.get(cfg.name) is not None:
         log(f"measured risk-controlled rollout ({S} steps) ...")
