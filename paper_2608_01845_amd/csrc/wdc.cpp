@@ -334,7 +334,7 @@ wdc_status mod_gemv(wdc_ctx *c, const std::string &name, int64_t off) {
 
 // The projection buffer is free while attention runs (q, k and v^T are in
 // their own buffers by then): scratch for the split of the last round.
-void attn_scratch(wdc_ctx *c, AttnArgs &a) {
+void attn_scratch(const wdc_ctx *c, AttnArgs &a) {
   a.part = c->ws ? (float *)c->qkv : nullptr;
   a.part_bytes = c->ws ? c->qkv_bytes : 0;
   a.force_splits = c->attn_splits;
@@ -1597,7 +1597,7 @@ wdc_status wdc_attention_plan(const wdc_ctx *ctx, int64_t n, int32_t *qb_main, i
   a.n_pad = attn_pad(n);
   a.heads = ctx->H;
   a.hd = ctx->hd;
-  attn_scratch(const_cast<wdc_ctx *>(ctx), a);
+  attn_scratch(ctx, a);
   if (ctx->d.dtype == WDC_BF16) {
     attn_split_plan(a);
   } else {
