@@ -606,7 +606,11 @@ def main():
                     "attention_tflops": round(att_tflops, 1) if att_tflops else None,
                     "gemm_ms_total": round(gemm_ms, 1), "gemm_launches": gemm_n,
                     "linear_tflops": round(gemm_tflops, 1) if gemm_tflops else None,
-                    "layernorm_modulate": hbm_entry(norm_ms, norm_n, norm_work)},
+                    "layernorm_modulate": hbm_entry(norm_ms, norm_n, norm_work),
+                    # query blocks of 256 per head over all keys, and the key ranges each
+                    # block of the last, partial dispatch round runs as (1: no split)
+                    "attention_plan": dict(zip(("query_blocks_over_all_keys", "key_ranges_of_the_rest"),
+                                               ctx.attention_plan(cfg.n_tokens)))},
         "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL.get(cfg.head_dim),
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
