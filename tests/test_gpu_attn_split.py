@@ -87,3 +87,41 @@ def test_whole_rounds_and_split_round_in_one_launch(head_dim):
     assert np.array_equal(got[:32 * 256], unsplit[:32 * 256])
     # the split rows differ from the unsplit ones by the bf16 roundings only
     assert diff <= 5e-3
+
+
+def test_batched_forward_with_split_round():
+    """A two-sample batched forward of the mid-size model (2 x 16 heads of 11
+    query blocks: 8 per head fill whole rounds, the other 3 x 32 run as 3 key
+    ranges, forced) against the same forward with the split switched off, and
+    one sample against the oracle."""
+    torch = torch_cuda()
+    import paper_2608_01845_amd as wdc
+    import synth
+    from tests.gpu_util import TOL_BF16_FINAL
+    from tests.test_gpu_batch import inputs
+    cfg = synth.get_config("mid")
+    ctxs = []
+    for splits in (3, 1):
+        os.environ["WDC_ATTN_SPLITS"] = str(splits)
+        try:
+            ctxs.append(wdc.Context(cfg, max_batch=2, allocate_weights=not ctxs))
+        finally:
+            del os.environ["WDC_ATTN_SPLITS"]
+    split, whole = ctxs
+    W = synth.gen_weights(cfg)
+    split.load_weights(W)
+    whole.bind_weights(split.weights)
+    host, dev = inputs(split, cfg, 2)
+    zs = [d["z_T"] for d in dev]
+    conds = [d["cond"] for d in dev]
+    a = split.forward_batch(zs, 0.7, conds)
+    b = whole.forward_batch(zs, 0.7, conds)
+    for i in range(2):
+        diff = rel_l2(a[i].cpu().numpy(), b[i].cpu().numpy())
+        print(f"sample {i}: split vs unsplit rel_l2 {diff:.2e}")
+        assert torch.isfinite(a[i]).all() and diff <= 1e-2
+    assert not all(torch.equal(a[i], b[i]) for i in range(2))      # the split ran
+    ref = dit.dit_forward(W, cfg, host[1]["z_T"], 0.7, host[1].get("cond"))
+    err = rel_l2(a[1].cpu().numpy(), ref)
+    print(f"sample 1 vs oracle {err:.2e}")
+    assert err <= TOL_BF16_FINAL
