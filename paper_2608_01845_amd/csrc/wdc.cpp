@@ -264,16 +264,28 @@ WsLayout ws_layout(const wdc_ctx *c) {
 template <typename F>
 hipError_t timed(wdc_ctx *c, int cls, double work, F &&fn) {
   if (!c->timing) return fn();
-  c->t_work[cls] += work;
-  TimedEvent ev;
+  TimedEvent ev{};
   ev.cls = cls;
-  hipEventCreate(&ev.a);
-  hipEventCreate(&ev.b);
-  hipEventRecord(ev.a, c->stream);
-  hipError_t e = fn();
-  hipEventRecord(ev.b, c->stream);
-  c->events.push_back(ev);
-  return e;
+  hipError_t e = hipEventCreate(&ev.a);
+  if (e != hipSuccess) return e;
+  if ((e = hipEventCreate(&ev.b)) != hipSuccess || (e = hipEventRecord(ev.a, c->stream)) != hipSuccess) {
+    (void)hipEventDestroy(ev.a);
+    if (ev.b) (void)hipEventDestroy(ev.b);
+    return e;
+  }
+  e = fn();
+  const hipError_t r = hipEventRecord(ev.b, c->stream);
+  c->events.push_back(ev);  // released by wdc_timing, wdc_set_timing or wdc_destroy
+  c->t_work[cls] += work;
+  return e != hipSuccess ? e : r;
+}
+
+void release_events(wdc_ctx *c) {
+  for (auto &e : c->events) {
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  c->events.clear();
 }
 
 // ---------------------------------------------------------------- kernel wrappers
@@ -1159,10 +1171,7 @@ wdc_status wdc_create(const wdc_model_desc *desc, const wdc_params *params, wdc_
 
 wdc_status wdc_destroy(wdc_ctx *ctx) {
   if (!ctx) return WDC_E_ARG;
-  for (auto &e : ctx->events) {
-    hipEventDestroy(e.a);
-    hipEventDestroy(e.b);
-  }
+  release_events(ctx);
   delete ctx;
   return WDC_OK;
 }
@@ -1334,7 +1343,7 @@ wdc_status wdc_state_reset(wdc_state *st, const float *h_cam) {
 
 wdc_status wdc_state_destroy(wdc_state *st) {
   if (!st) return WDC_E_ARG;
-  if (st->h_red) hipHostFree(st->h_red);
+  if (st->h_red) (void)hipHostFree(st->h_red);
   delete st;
   return WDC_OK;
 }
@@ -1618,11 +1627,7 @@ wdc_status wdc_linear(wdc_ctx *ctx, const void *d_a, int64_t lda, const void *d_
 wdc_status wdc_set_timing(wdc_ctx *ctx, int32_t on) {
   if (!ctx) return WDC_E_ARG;
   ctx->timing = on != 0;
-  for (auto &e : ctx->events) {
-    hipEventDestroy(e.a);
-    hipEventDestroy(e.b);
-  }
-  ctx->events.clear();
+  release_events(ctx);
   for (int i = 0; i < WDC_T_COUNT; ++i) {
     ctx->t_ms[i] = 0;
     ctx->t_cnt[i] = 0;
@@ -1637,13 +1642,16 @@ wdc_status wdc_timing(wdc_ctx *ctx, double out_ms[WDC_T_COUNT], int64_t out_coun
   HIPCHK(ctx, hipStreamSynchronize(ctx->stream));
   for (auto &e : ctx->events) {
     float ms = 0;
-    HIPCHK(ctx, hipEventElapsedTime(&ms, e.a, e.b));
+    const hipError_t err = hipEventElapsedTime(&ms, e.a, e.b);
+    if (err != hipSuccess) {
+      set_err(ctx, "hipEventElapsedTime failed: %s", hipGetErrorString(err));
+      release_events(ctx);
+      return WDC_E_HIP;
+    }
     ctx->t_ms[e.cls] += ms;
     ctx->t_cnt[e.cls] += 1;
-    hipEventDestroy(e.a);
-    hipEventDestroy(e.b);
   }
-  ctx->events.clear();
+  release_events(ctx);
   for (int i = 0; i < WDC_T_COUNT; ++i) {
     out_ms[i] = ctx->t_ms[i];
     out_count[i] = ctx->t_cnt[i];
