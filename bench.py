@@ -611,7 +611,11 @@ def main():
                     # block of the last, partial dispatch round runs as (1: no split)
                     "attention_plan": dict(zip(("query_blocks_over_all_keys", "key_ranges_of_the_rest"),
                                                ctx.attention_plan(cfg.n_tokens)))},
-        "roofline": {"bound": "mfma", "kernel": ATTN_KERNEL.get(cfg.head_dim),
+        "roofline": {"bound": "mfma",
+                     # one attention call: the kernel, plus the combine launch when its last
+                     # dispatch round runs as key-range splits
+                     "kernel": ATTN_KERNEL.get(cfg.head_dim) + (
+                         f" + k_attn_combine<{cfg.head_dim}>" if ctx.attention_plan(cfg.n_tokens)[1] > 1 else ""),
                      "achieved": round(att_tflops, 1) if att_tflops else None,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4) if att_tflops else None,
