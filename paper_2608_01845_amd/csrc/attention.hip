@@ -18,7 +18,11 @@
 //    (k_attn_bf16_ppr3);
 //  * one head's padded q, k and v^T rows are addressed with 32-bit byte
 //    offsets (buffer ranges, tile offsets): at most 2^30 B per head, which
-//    the library checks before launching (attn_len_ok).
+//    the library checks before launching (attn_len_ok);
+//  * the query blocks of the last, partly filled dispatch round can run as
+//    several blocks over disjoint key ranges in the same launch, each leaving
+//    its unnormalised rows, reference maxima and row sums in scratch for a
+//    second launch that combines them in range order (attn_split_plan).
 // float32 path: a plain online-softmax kernel (tiny fp32 workload).
 #include "common.h"
 
