@@ -13,7 +13,7 @@
 // products take an XCD-aware block order, and long-K ones whose last dispatch
 // round would be thin run their last rows as a second launch of 128 x 128 tiles;
 // products too small to fill one dispatch round of 256 x 256 tiles run on
-// 128 x 128 tiles throughout.
+// 128 x 128 tiles throughout (128 x 64 when even those would not fill it).
 // float32 path (tiny fp32 workload, and shapes the MFMA tiles do not cover):
 // a plain LDS-tiled FMA kernel.
 #include "common.h"
@@ -844,8 +844,16 @@ hipError_t launch_gemm(int dtype, const GemmArgs &g_in, hipStream_t s) {
     // A product that would leave compute units idle in its only dispatch round
     // (the mid-size model's products: 44 to 176 tiles of 256 x 256) runs four
     // times the blocks on 128 x 128 tiles: 17% off the mid-size forward, whose
-    // q/k/v projection then takes the separate preparation kernels.
-    if (small_product(g)) return launch_mfma<128, 128, 2, 2>(g, s);
+    // q/k/v projection then takes the separate preparation kernels. One that
+    // would still leave CUs idle on 128 x 128 tiles (its N = 1,024 products:
+    // 168 tiles) runs on 128 x 64 tiles, up to two blocks per CU: 5.7% off the
+    // mid-size forward's products. Every output is summed over K in the same
+    // order on any tile shape, so the results are the same bits.
+    if (small_product(g)) {
+      const int64_t t128 = (g.m + 127) / 128 * (g.n / 128) * (g.batch > 1 ? g.batch : 1);
+      if (t128 < device_cus()) return launch_mfma<128, 64, 2, 2>(g, s);
+      return launch_mfma<128, 128, 2, 2>(g, s);
+    }
     if (g.n % 256 == 0 && g.m >= 512 && out16) {
       // Tail split for a single large long-K product on a 256-CU device: the
       // rows whose 256 x 256 tiles fill whole dispatch rounds (m1 tiles, a
