@@ -37,14 +37,15 @@ def _pair(cfg, max_batch=1):
     return fused, sep
 
 
-@pytest.mark.parametrize("head_dim", [64, 128])
-def test_fused_qkv_blocks_equal_separate_preparation(head_dim):
+@pytest.mark.parametrize("head_dim,rope", [(64, True), (128, True), (64, False), (128, False)])
+def test_fused_qkv_blocks_equal_separate_preparation(head_dim, rope):
     """560 video + 21 text tokens: the sequential and single blocks and the
     dual block's video stream take the fused epilogue (the 21 text rows of the
     dual block stay on the separate kernels); the last 256-row tile is partial
-    and its last group of 16 tokens incomplete."""
+    and its last group of 16 tokens incomplete. Without rotary dimensions the
+    epilogue takes its form without rotation-table reads."""
     torch = torch_cuda()
-    cfg = small_cfg("bf16", head_dim=head_dim, latent=(16, 4, 20, 28))
+    cfg = small_cfg("bf16", head_dim=head_dim, latent=(16, 4, 20, 28), **({} if rope else {"rope": (0, 0, 0)}))
     fused, sep = _pair(cfg)
     x = synth.gen_block_input(cfg)
     c = torch.from_numpy(synth.gen_cemb(cfg)).cuda()
