@@ -746,7 +746,9 @@ hipError_t launch_mfma(const GemmArgs &g0, hipStream_t s) {
   // 8 x 4 rectangles. 2 x 16 ones (A panels, larger than the last-level cache,
   // re-read once per rectangle column; weight panels, which fit it, once per
   // rectangle row) made the N = 12,288 product 2.5-3% faster alone but the
-  // whole 13B forward's GEMMs 1% slower (same-box A/B), so they are not used.
+  // whole 13B forward's GEMMs 1% slower (same-box A/B), so they are not used;
+  // nor 2 x 16 for that product alone (1.1% slower over the forward) or 16 x 2
+  // for the N = 3,072 ones (1.8% slower).
   g.rect_n = 4;
   const int chunks = n_tiles % g.rect_n == 0 ? (m_tiles + 32 / g.rect_n - 1) / (32 / g.rect_n) * (n_tiles / g.rect_n) : 0;
   g.order = (BM == 256 && chunks >= 64 && g.batch <= 1 && device_cus() == 256) ? 1 : 0;
